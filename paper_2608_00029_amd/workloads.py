@@ -1,0 +1,87 @@
+"""Seeded synthetic inputs for the attention workloads.
+
+This module only draws random numbers; it holds none of attention's
+arithmetic, and both the HIP path's callers and the CPU reference's callers
+take their inputs from here.
+
+Recipe (identical for every caller): a CPU ``torch.Generator`` seeded with
+``seed`` draws float32 ``randn`` tensors of shape [B, H, S, D] in the order
+Q, K, V, dO; Q and K are then multiplied by ``qk_sigma``; for bf16 workloads
+every tensor is rounded to bfloat16 (round-to-nearest-even, torch's ``.to``).
+The values stand in for the attention activations of GPT-2 124M training
+(12 heads of dimension 64 at a 1024-token context, the model of the paper's
+Table 4, at the batch of 8 sequences its section 6.1 says it trains with);
+the paper's training data is not used.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    S: int
+    D: int
+    scale: float
+    dtype: str          # "f32" or "bf16": storage dtype of Q, K, V, O, dO, dQ, dK, dV
+    qk_sigma: float     # standard deviation of Q and K entries
+    seed: int
+    causal: bool = True
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return torch.float32 if self.dtype == "f32" else torch.bfloat16
+
+    @property
+    def pairs(self) -> int:
+        """Number of (query, key) pairs the mask keeps, summed over B*H."""
+        per_head = self.S * (self.S + 1) // 2 if self.causal else self.S * self.S
+        return self.B * self.H * per_head
+
+    def counted_flops(self) -> tuple[float, float]:
+        """Causal FLOP count used for throughput: fwd 2*B*H*S^2*D, bwd 5*B*H*S^2*D
+        (half of the dense 4*B*H*S^2*D and 10*B*H*S^2*D); dense counts when not causal."""
+        base = self.B * self.H * self.S * self.S * self.D
+        f = 1.0 if self.causal else 2.0
+        return 2.0 * base * f, 5.0 * base * f
+
+
+SEED_BASE = 1234
+
+WORKLOADS = [
+    Workload("tiny_f32_B1_H2_S128_D64", 1, 2, 128, 64, 1.0 / 8.0, "f32", 1.0, SEED_BASE + 0),
+    Workload("gpt2_small_B8_H12_S1024_D64", 8, 12, 1024, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 1),
+    Workload("gpt2_medium_B8_H16_S1024_D64", 8, 16, 1024, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 2),
+    Workload("gpt2_xl_width_B4_H25_S1024_D64", 4, 25, 1024, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 3),
+    Workload("long_ctx_B2_H16_S4096_D128", 2, 16, 4096, 128, 1.0 / math.sqrt(128.0), "bf16", 3.0,
+             SEED_BASE + 4),
+]
+
+BY_NAME = {w.name: w for w in WORKLOADS}
+
+
+def make_inputs(B: int, H: int, S: int, D: int, dtype: str = "bf16", seed: int = SEED_BASE,
+                qk_sigma: float = 1.0):
+    """Return (q, k, v, do) CPU tensors, contiguous [B, H, S, D], in the storage dtype."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    shape = (B, H, S, D)
+    q = torch.randn(shape, generator=g, dtype=torch.float32)
+    k = torch.randn(shape, generator=g, dtype=torch.float32)
+    v = torch.randn(shape, generator=g, dtype=torch.float32)
+    do = torch.randn(shape, generator=g, dtype=torch.float32)
+    if qk_sigma != 1.0:
+        q = q * qk_sigma
+        k = k * qk_sigma
+    td = torch.float32 if dtype == "f32" else torch.bfloat16
+    return tuple(t.to(td).contiguous() for t in (q, k, v, do))
+
+
+def workload_inputs(w: Workload):
+    return make_inputs(w.B, w.H, w.S, w.D, w.dtype, w.seed, w.qk_sigma)
