@@ -1,0 +1,129 @@
+/*
+ * cattn.h -- C ABI of the MI355X (gfx950) fused causal multi-head attention
+ * library: forward (O, LSE) and backward (dQ, dK, dV).
+ *
+ * What is computed (Nova paper, section 4.2 "Attention as a First-Class
+ * Lowering", and its backward paragraph): for every batch b and head h,
+ *
+ *     S   = scale * Q K^T                  scores, never written to memory
+ *     S[i,j] excluded for j > i            when causal (the diagonal is kept)
+ *     LSE = log(sum_j exp(S[i,j]))         per row, natural log
+ *     P   = exp(S - LSE)
+ *     O   = P V
+ *
+ * and, for an upstream gradient dO, with D = rowsum(dO * O):
+ *
+ *     dV = P^T dO,  dS = P * (dO V^T - D),  dQ = scale * dS K,  dK = scale * dS^T Q
+ *
+ * The forward streams key/value tiles through an online (running max / running
+ * sum) base-2 softmax and keeps S and P in registers; the backward recomputes P
+ * from LSE in two kernels -- one reduces over keys (dQ, and writes D), one over
+ * queries (dK, dV) -- so the S x S matrix never reaches HBM in either direction
+ * and no atomics are used (results are bitwise reproducible).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors Q, K, V, O, dO, dQ, dK, dV are contiguous row-major [B, H, S, D]
+ *    arrays of the element type `dtype` (CATTN_F32: IEEE float; CATTN_BF16:
+ *    bfloat16 stored as 16-bit words).  LSE and the workspace are float arrays
+ *    [B, H, S].  Queries and keys share the sequence length S.
+ *  - Every pointer is a DEVICE pointer on the current HIP device, allocated and
+ *    freed by the caller; the library allocates nothing and keeps no state
+ *    between calls, so concurrent calls on different streams are safe as long
+ *    as their output buffers do not overlap.
+ *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Calls only
+ *    enqueue work and return; there is no host synchronisation.  Results are
+ *    ready when the stream reaches that point.
+ *  - Precision: CATTN_BF16 multiplies bf16 operands on the matrix cores with
+ *    float accumulation; P and dS are rounded to bf16 (round to nearest even)
+ *    before they enter a contraction; softmax statistics, LSE, D and all
+ *    accumulators are float.  CATTN_F32 runs every contraction in float.
+ *  - Supported shapes: D in {64, 128}; any S >= 1 with S * D <= 2^30 (a ragged
+ *    last tile is handled in the kernels); B * H * ceil(S / 128) < 2^31.
+ *    B, H or S equal to 0 is an empty problem: the call returns CATTN_OK and
+ *    touches no memory (pointers may then be NULL).
+ *  - `scale` must be finite and > 0 (the softmax scale, e.g. 1/sqrt(D)).
+ *  - `causal` != 0 selects the causal mask; 0 attends to every key.
+ *
+ * Errors: argument errors are detected on the host before anything is
+ * enqueued and leave every buffer untouched.  CATTN_ERR_HIP means a launch was
+ * rejected by the HIP runtime; cattn_last_error_string() then names the HIP
+ * error (per calling thread).
+ */
+#ifndef CATTN_H
+#define CATTN_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CATTN_OK = 0,
+  CATTN_ERR_INVALID_ARG = 1,  /* NULL pointer, negative size, bad dtype, scale <= 0
+                                 or not finite, an output overlapping an input */
+  CATTN_ERR_UNSUPPORTED = 2,  /* valid but not implemented: D not in {64, 128},
+                                 S * D > 2^30, grid too large */
+  CATTN_ERR_HIP = 3           /* the HIP runtime rejected a launch */
+} cattn_status;
+
+typedef enum {
+  CATTN_F32 = 0,
+  CATTN_BF16 = 1
+} cattn_dtype;
+
+/*
+ * Forward pass (section 4.2: online softmax over key tiles, base-2 exponent
+ * with the scale folded in, finite mask sentinel, causal loop clamping, LSE
+ * saved per row).
+ *
+ *   q, k, v : in,  [B, H, S, D] `dtype`
+ *   o       : out, [B, H, S, D] `dtype`   (must not overlap q, k, v or lse)
+ *   lse     : out, [B, H, S] float, natural-log log-sum-exp of each row of
+ *             scale * Q K^T over the visible keys (must not overlap q, k, v, o)
+ */
+cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v,
+                            void* o, float* lse,
+                            int B, int H, int S, int D,
+                            float scale, int causal, int dtype, void* stream);
+
+/*
+ * Backward pass (section 4.2, backward paragraph: two fused kernels that
+ * recompute P from the saved LSE -- a dQ kernel reducing over keys, which
+ * also forms D = rowsum(dO * O) in float from the given O, then a dK/dV kernel
+ * reducing over queries; the loop bounds are clamped to the causal triangle).
+ *
+ *   q, k, v  : in, [B, H, S, D] `dtype` -- the forward's inputs
+ *   o        : in, [B, H, S, D] `dtype` -- the forward's output
+ *   dout     : in, [B, H, S, D] `dtype` -- upstream gradient dO
+ *   lse      : in, [B, H, S] float      -- the forward's LSE (natural log)
+ *   dq,dk,dv : out, [B, H, S, D] `dtype` (must not overlap any input, each
+ *              other, or the workspace)
+ *   workspace: scratch of at least cattn_bwd_workspace_bytes(B, H, S, D)
+ *              bytes, 4-byte aligned; on return it holds D as float [B, H, S].
+ *              Its prior contents are ignored.
+ *   scale, causal: the values the forward was called with.
+ */
+cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
+                            const void* o, const void* dout, const float* lse,
+                            void* dq, void* dk, void* dv, float* workspace,
+                            int B, int H, int S, int D,
+                            float scale, int causal, int dtype, void* stream);
+
+/* Bytes of workspace cattn_attn_bwd needs: B * H * S * sizeof(float)
+ * (0 for an empty or invalid shape). */
+size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);
+
+/* Static, NUL-terminated name of a status code ("unknown status" otherwise). */
+const char* cattn_status_string(int status);
+
+/* Description of the last CATTN_ERR_HIP / argument error on the calling
+ * thread ("" if none).  Valid until the next call on the same thread. */
+const char* cattn_last_error_string(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CATTN_H */

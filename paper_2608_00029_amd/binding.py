@@ -1,0 +1,173 @@
+"""Thin ctypes binding over the C ABI of libcattn.so (include/cattn.h).
+
+Argument marshalling only: tensors are checked for device, dtype, layout and
+shape, outputs are allocated with torch when the caller does not pass them,
+and the raw device pointers plus torch's current HIP stream are handed to the
+library.  Every step of attention runs in the library's HIP kernels; if the
+library is not built this module raises instead of computing anything.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcattn.so")
+_lib: Optional[ctypes.CDLL] = None
+
+CATTN_OK, CATTN_ERR_INVALID_ARG, CATTN_ERR_UNSUPPORTED, CATTN_ERR_HIP = 0, 1, 2, 3
+CATTN_F32, CATTN_BF16 = 0, 1
+
+EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_bwd_workspace_bytes", "cattn_status_string",
+            "cattn_last_error_string")
+
+
+class CattnError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}: {detail}")
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load libcattn.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"HIP attention library not built: {_LIB_PATH} is missing "
+                               "(run __graft_entry__.build() or python -m paper_2608_00029_amd.build)")
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+        L.cattn_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
+        L.cattn_attn_fwd.restype = i
+        L.cattn_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
+        L.cattn_attn_bwd.restype = i
+        L.cattn_bwd_workspace_bytes.argtypes = [i, i, i, i]
+        L.cattn_bwd_workspace_bytes.restype = ctypes.c_size_t
+        L.cattn_status_string.argtypes = [i]
+        L.cattn_status_string.restype = ctypes.c_char_p
+        L.cattn_last_error_string.argtypes = []
+        L.cattn_last_error_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().cattn_status_string(int(status)).decode()
+
+
+def last_error_string() -> str:
+    return lib().cattn_last_error_string().decode()
+
+
+def workspace_bytes(B: int, H: int, S: int, D: int) -> int:
+    return int(lib().cattn_bwd_workspace_bytes(B, H, S, D))
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return CATTN_F32
+    if t.dtype == torch.bfloat16:
+        return CATTN_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}: use float32 or bfloat16")
+
+
+def _check(name: str, t: torch.Tensor, shape, dtype, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if t.numel() and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous [B, H, S, D]")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr() if t is not None and t.numel() else 0)
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def attn_fwd(q, k, v, scale: float, causal: bool = True, o=None, lse=None):
+    """O, LSE = attention forward of contiguous [B, H, S, D] tensors on a HIP device.
+
+    LSE is float32 [B, H, S] in natural-log units.  `o` / `lse` may be passed
+    to write into existing buffers.  Enqueued on torch's current stream.
+    """
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, S, D]")
+    B, H, S, D = q.shape
+    if q.device.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    for n, t in (("q", q), ("k", k), ("v", v)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, S), dtype=torch.float32, device=q.device)
+    _check("o", o, q.shape, q.dtype, q.device)
+    _check("lse", lse, (B, H, S), torch.float32, q.device)
+    st = lib().cattn_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, S, D, float(scale),
+                              int(bool(causal)), _dtype_code(q), _stream(q.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_attn_fwd", last_error_string())
+    return o, lse
+
+
+def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk=None, dv=None,
+             workspace=None):
+    """dQ, dK, dV of attention for upstream gradient `do`, given the forward's O and LSE.
+
+    `workspace` (float32, >= B*H*S elements) receives D = rowsum(dO * O).
+    """
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, S, D]")
+    B, H, S, D = q.shape
+    if q.device.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    _check("lse", lse, (B, H, S), torch.float32, q.device)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    if workspace is None:
+        workspace = torch.empty((B * H * S,), dtype=torch.float32, device=q.device)
+    if workspace.dtype != torch.float32 or workspace.device != q.device or not workspace.is_contiguous() \
+            or workspace.numel() < B * H * S:
+        raise ValueError("workspace must be a contiguous float32 tensor of >= B*H*S elements on q's device")
+    st = lib().cattn_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq), _ptr(dk),
+                              _ptr(dv), _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)),
+                              _dtype_code(q), _stream(q.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_attn_bwd", last_error_string())
+    return dq, dk, dv
+
+
+def raw_fwd(q_ptr: int, k_ptr: int, v_ptr: int, o_ptr: int, lse_ptr: int, B: int, H: int, S: int, D: int,
+            scale: float, causal: int, dtype: int, stream: int = 0) -> int:
+    """Direct C-ABI call with integer pointers (returns the status code)."""
+    vp = ctypes.c_void_p
+    return lib().cattn_attn_fwd(vp(q_ptr), vp(k_ptr), vp(v_ptr), vp(o_ptr), vp(lse_ptr), B, H, S, D,
+                                float(scale), int(causal), int(dtype), vp(stream))
+
+
+def raw_bwd(q_ptr, k_ptr, v_ptr, o_ptr, do_ptr, lse_ptr, dq_ptr, dk_ptr, dv_ptr, ws_ptr, B, H, S, D,
+            scale: float, causal: int, dtype: int, stream: int = 0) -> int:
+    vp = ctypes.c_void_p
+    return lib().cattn_attn_bwd(vp(q_ptr), vp(k_ptr), vp(v_ptr), vp(o_ptr), vp(do_ptr), vp(lse_ptr),
+                                vp(dq_ptr), vp(dk_ptr), vp(dv_ptr), vp(ws_ptr), B, H, S, D, float(scale),
+                                int(causal), int(dtype), vp(stream))

@@ -1,0 +1,45 @@
+// Host-side launchers of the attention kernels (internal to the library; the
+// public interface is the C ABI in cattn.h).  Arguments are validated by the
+// caller before any launcher runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cattn {
+
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  int BH, S, D;
+  float scale;
+  bool causal;
+  bool bf16;
+};
+
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dout;
+  const float* lse;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dvec;  // D = rowsum(dO * O), [BH, S] float
+  int BH, S, D;
+  float scale;
+  bool causal;
+  bool bf16;
+};
+
+hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
+int64_t fwd_grid_blocks(int BH, int S);
+int64_t bwd_grid_blocks(int BH, int S);
+
+}  // namespace cattn

@@ -1,0 +1,131 @@
+// C ABI entry points (declared and documented in include/cattn.h): argument
+// validation on the host, then dispatch to the kernel launchers on the
+// caller's stream.  Nothing is allocated and no state survives a call except
+// the per-thread text of the last error.
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/cattn.h"
+#include "attn_launch.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+cattn_status fail(cattn_status st, const char* msg) {
+  snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
+  return st;
+}
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void* p, size_t bytes) {
+  const uintptr_t a = (uintptr_t)p;
+  return Range{a, a + bytes};
+}
+
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Shape checks shared by both entry points.  Returns CATTN_OK with *empty set
+// when the problem is empty.
+cattn_status check_shape(int B, int H, int S, int D, float scale, int dtype, bool* empty) {
+  *empty = false;
+  if (B < 0 || H < 0 || S < 0) return fail(CATTN_ERR_INVALID_ARG, "negative B, H or S");
+  if (D <= 0) return fail(CATTN_ERR_INVALID_ARG, "D must be positive");
+  if (dtype != CATTN_F32 && dtype != CATTN_BF16) return fail(CATTN_ERR_INVALID_ARG, "dtype must be CATTN_F32 or CATTN_BF16");
+  if (!(scale > 0.f) || !isfinite(scale)) return fail(CATTN_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (D != 64 && D != 128) return fail(CATTN_ERR_UNSUPPORTED, "head dimension D must be 64 or 128");
+  if (B == 0 || H == 0 || S == 0) {
+    *empty = true;
+    return CATTN_OK;
+  }
+  if ((int64_t)S * D > (int64_t(1) << 30)) return fail(CATTN_ERR_UNSUPPORTED, "S * D exceeds 2^30");
+  if ((int64_t)B * H > INT32_MAX) return fail(CATTN_ERR_UNSUPPORTED, "B * H exceeds 2^31 - 1");
+  const int64_t BH = (int64_t)B * H;
+  if (cattn::fwd_grid_blocks((int)BH, S) >= (int64_t(1) << 31) || cattn::bwd_grid_blocks((int)BH, S) >= (int64_t(1) << 31))
+    return fail(CATTN_ERR_UNSUPPORTED, "grid too large");
+  return CATTN_OK;
+}
+
+cattn_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return CATTN_OK;
+  snprintf(g_last_error, sizeof(g_last_error), "HIP error %d: %s", (int)e, hipGetErrorString(e));
+  return CATTN_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S,
+                            int D, float scale, int causal, int dtype, void* stream) {
+  g_last_error[0] = '\0';
+  bool empty;
+  cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
+  if (st != CATTN_OK || empty) return st;
+  if (!q || !k || !v || !o || !lse) return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  const size_t esz = dtype == CATTN_BF16 ? 2 : 4;
+  const size_t n = (size_t)B * H * S * D, nrow = (size_t)B * H * S;
+  const Range rq = range_of(q, n * esz), rk = range_of(k, n * esz), rv = range_of(v, n * esz);
+  const Range ro = range_of(o, n * esz), rl = range_of(lse, nrow * 4);
+  for (Range out : {ro, rl})
+    for (Range in : {rq, rk, rv})
+      if (overlap(out, in)) return fail(CATTN_ERR_INVALID_ARG, "an output overlaps an input");
+  if (overlap(ro, rl)) return fail(CATTN_ERR_INVALID_ARG, "o overlaps lse");
+
+  cattn::FwdArgs a{q, k, v, o, lse, B * H, S, D, scale, causal != 0, dtype == CATTN_BF16};
+  (void)hipGetLastError();  // do not report an earlier, unrelated error as ours
+  return hip_status(cattn::launch_fwd(a, (hipStream_t)stream));
+}
+
+cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                            const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H, int S,
+                            int D, float scale, int causal, int dtype, void* stream) {
+  g_last_error[0] = '\0';
+  bool empty;
+  cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
+  if (st != CATTN_OK || empty) return st;
+  if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv || !workspace)
+    return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  if (((uintptr_t)workspace & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "workspace must be 4-byte aligned");
+  const size_t esz = dtype == CATTN_BF16 ? 2 : 4;
+  const size_t n = (size_t)B * H * S * D, nrow = (size_t)B * H * S;
+  const Range ins[] = {range_of(q, n * esz), range_of(k, n * esz), range_of(v, n * esz), range_of(o, n * esz),
+                       range_of(dout, n * esz), range_of(lse, nrow * 4)};
+  const Range outs[] = {range_of(dq, n * esz), range_of(dk, n * esz), range_of(dv, n * esz),
+                        range_of(workspace, nrow * 4)};
+  for (const Range& out : outs)
+    for (const Range& in : ins)
+      if (overlap(out, in)) return fail(CATTN_ERR_INVALID_ARG, "an output or the workspace overlaps an input");
+  for (int i = 0; i < 4; ++i)
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], outs[j])) return fail(CATTN_ERR_INVALID_ARG, "outputs or workspace overlap each other");
+
+  cattn::BwdArgs a{q, k, v, o, dout, lse, dq, dk, dv, workspace, B * H, S, D, scale, causal != 0,
+                   dtype == CATTN_BF16};
+  (void)hipGetLastError();
+  return hip_status(cattn::launch_bwd(a, (hipStream_t)stream));
+}
+
+size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D) {
+  if (B <= 0 || H <= 0 || S <= 0 || D <= 0) return 0;
+  return (size_t)B * H * S * sizeof(float);
+}
+
+const char* cattn_status_string(int status) {
+  switch (status) {
+    case CATTN_OK: return "CATTN_OK";
+    case CATTN_ERR_INVALID_ARG: return "CATTN_ERR_INVALID_ARG";
+    case CATTN_ERR_UNSUPPORTED: return "CATTN_ERR_UNSUPPORTED";
+    case CATTN_ERR_HIP: return "CATTN_ERR_HIP";
+    default: return "unknown status";
+  }
+}
+
+const char* cattn_last_error_string(void) { return g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+"""The C-ABI library loads on a host without a GPU, exports every symbol that
+include/cattn.h declares, and rejects bad arguments on the host before any
+HIP call (no kernel is launched by these tests)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_00029_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cattn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cattn_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(b.library_path()):
+        pytest.fail("libcattn.so is not built (run __graft_entry__.build())")
+    return b.lib()
+
+
+def test_header_declares_expected_entry_points():
+    assert declared_functions() == sorted(b.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_status_strings(lib):
+    assert b.status_string(0) == "CATTN_OK"
+    assert b.status_string(1) == "CATTN_ERR_INVALID_ARG"
+    assert b.status_string(2) == "CATTN_ERR_UNSUPPORTED"
+    assert b.status_string(3) == "CATTN_ERR_HIP"
+    assert b.status_string(77) == "unknown status"
+
+
+def test_workspace_bytes(lib):
+    assert b.workspace_bytes(8, 12, 1024, 64) == 8 * 12 * 1024 * 4
+    assert b.workspace_bytes(0, 12, 1024, 64) == 0
+    assert b.workspace_bytes(-1, 12, 1024, 64) == 0
+
+
+# Fake, non-NULL "device" addresses: every case below is rejected on the host
+# before anything is enqueued, so they are never dereferenced.
+P = [0x10000000 * (i + 1) for i in range(10)]
+
+
+@pytest.mark.parametrize("args,status", [
+    ((1, 1, 16, 64, 0.125, 1, 1), b.CATTN_OK),              # valid shape, but NULL pointers below
+    ((-1, 1, 16, 64, 0.125, 1, 1), b.CATTN_ERR_INVALID_ARG),
+    ((1, 1, 16, 0, 0.125, 1, 1), b.CATTN_ERR_INVALID_ARG),
+    ((1, 1, 16, 64, 0.125, 1, 7), b.CATTN_ERR_INVALID_ARG),   # bad dtype
+    ((1, 1, 16, 64, 0.0, 1, 1), b.CATTN_ERR_INVALID_ARG),     # scale must be > 0
+    ((1, 1, 16, 64, float("nan"), 1, 1), b.CATTN_ERR_INVALID_ARG),
+    ((1, 1, 16, 64, float("inf"), 1, 1), b.CATTN_ERR_INVALID_ARG),
+    ((1, 1, 16, 96, 0.125, 1, 1), b.CATTN_ERR_UNSUPPORTED),   # D not in {64, 128}
+    ((1, 1, 16, 32, 0.125, 1, 0), b.CATTN_ERR_UNSUPPORTED),
+    ((1, 1, 1 << 24, 128, 0.125, 1, 1), b.CATTN_ERR_UNSUPPORTED),  # S*D > 2^30
+])
+def test_fwd_argument_errors(lib, args, status):
+    st = b.raw_fwd(0, 0, 0, 0, 0, *args)
+    expected = b.CATTN_ERR_INVALID_ARG if status == b.CATTN_OK else status  # NULL pointers
+    assert st == expected, b.last_error_string()
+    assert b.last_error_string() != ""
+
+
+def test_empty_problem_is_a_noop(lib):
+    for B, H, S in ((0, 4, 16), (2, 0, 16), (2, 4, 0)):
+        assert b.raw_fwd(0, 0, 0, 0, 0, B, H, S, 64, 0.125, 1, 1) == b.CATTN_OK
+        assert b.raw_bwd(0, 0, 0, 0, 0, 0, 0, 0, 0, 0, B, H, S, 64, 0.125, 1, 1) == b.CATTN_OK
+
+
+def test_fwd_rejects_overlapping_output(lib):
+    B, H, S, D = 1, 2, 64, 64
+    n = B * H * S * D * 2
+    # o aliases q
+    assert b.raw_fwd(P[0], P[1], P[2], P[0], P[3], B, H, S, D, 0.125, 1, 1) == b.CATTN_ERR_INVALID_ARG
+    # lse starts inside v
+    assert b.raw_fwd(P[0], P[1], P[2], P[3], P[2] + n - 4, B, H, S, D, 0.125, 1, 1) == b.CATTN_ERR_INVALID_ARG
+    # o overlaps lse
+    assert b.raw_fwd(P[0], P[1], P[2], P[3], P[3] + 16, B, H, S, D, 0.125, 1, 1) == b.CATTN_ERR_INVALID_ARG
+
+
+def test_bwd_argument_errors(lib):
+    B, H, S, D = 1, 2, 64, 64
+    ok = dict(q=P[0], k=P[1], v=P[2], o=P[3], do=P[4], lse=P[5], dq=P[6], dk=P[7], dv=P[8], ws=P[9])
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return b.raw_bwd(a["q"], a["k"], a["v"], a["o"], a["do"], a["lse"], a["dq"], a["dk"], a["dv"], a["ws"],
+                         B, H, S, D, 0.125, 1, 1)
+
+    assert call(ws=0) == b.CATTN_ERR_INVALID_ARG
+    assert call(dq=P[0]) == b.CATTN_ERR_INVALID_ARG        # dq aliases q
+    assert call(dk=P[6]) == b.CATTN_ERR_INVALID_ARG        # dk aliases dq
+    assert call(ws=P[8] + 8) == b.CATTN_ERR_INVALID_ARG    # workspace inside dv
+    assert call(ws=P[9] + 2) == b.CATTN_ERR_INVALID_ARG    # misaligned workspace
+    assert b.raw_bwd(*[ok[k] for k in ("q", "k", "v", "o", "do", "lse", "dq", "dk", "dv", "ws")],
+                     B, H, S, 80, 0.125, 1, 1) == b.CATTN_ERR_UNSUPPORTED
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    q = torch.zeros(1, 1, 8, 64)
+    with pytest.raises(ValueError):
+        b.attn_fwd(q, q, q, 0.125)

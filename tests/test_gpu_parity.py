@@ -1,0 +1,177 @@
+"""Parity of the HIP attention path (through the C ABI) with the float64 oracle.
+
+Small cases compare every output element; they span several 128-row query
+tiles, 64-row key tiles and a ragged last tile, in both dtypes, both head
+dimensions, causal and not.  The five named workloads run at full size in the
+launch configuration the benchmark times and are compared on whole sampled
+(batch, head) slices, which the oracle computes exactly.  The backward is
+end-to-end: it consumes the GPU forward's O and LSE.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.attn_oracle as orc
+from paper_2608_00029_amd import attn_bwd, attn_fwd
+from paper_2608_00029_amd.workloads import WORKLOADS, make_inputs, workload_inputs
+from parity_util import check_tensor, say, to64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def gpu_fwd_bwd(q, k, v, do, scale, causal):
+    qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
+    o, lse = attn_fwd(qd, kd, vd, scale, causal)
+    dq, dk, dv = attn_bwd(qd, kd, vd, o, dod, lse, scale, causal)
+    torch.cuda.synchronize()
+    return tuple(t.cpu() for t in (o, lse, dq, dk, dv))
+
+
+def compare_all(dtype, got, q, k, v, do, scale, causal):
+    o, lse, dq, dk, dv = got
+    ro, rlse = orc.attn_fwd(q, k, v, scale, causal)
+    rdq, rdk, rdv = orc.attn_bwd(q, k, v, do, scale, causal)
+    rep = [check_tensor(n, dtype, g, r) for n, g, r in
+           (("o", o, ro), ("lse", lse, rlse), ("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv))]
+    print("  " + "  ".join(rep), flush=True)
+
+
+SMALL = [
+    # dtype, B, H, S, D, causal, qk_sigma
+    ("f32", 1, 2, 128, 64, True, 1.0),
+    ("f32", 1, 2, 128, 64, False, 1.0),
+    ("f32", 2, 1, 200, 64, True, 1.0),
+    ("f32", 1, 2, 333, 128, True, 1.0),
+    ("f32", 1, 1, 200, 128, False, 1.0),
+    ("bf16", 2, 3, 300, 64, True, 1.0),
+    ("bf16", 1, 2, 300, 128, True, 1.0),
+    ("bf16", 1, 2, 257, 64, False, 1.0),
+    ("bf16", 1, 1, 513, 128, False, 1.0),
+    ("bf16", 1, 2, 384, 128, True, 3.0),
+    ("bf16", 1, 2, 640, 64, True, 3.0),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "-".join(map(str, c)))
+def test_small_full_parity(cuda, case):
+    dtype, B, H, S, D, causal, sigma = case
+    scale = 1.0 / math.sqrt(D)
+    q, k, v, do = make_inputs(B, H, S, D, dtype, seed=777 + S + D, qk_sigma=sigma)
+    say(f"small {case}")
+    got = gpu_fwd_bwd(q, k, v, do, scale, causal)
+    compare_all(dtype, got, q, k, v, do, scale, causal)
+
+
+EDGE_S = [1, 2, 31, 32, 33, 63, 64, 65, 127, 129]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("S", EDGE_S)
+def test_edge_lengths(cuda, dtype, S):
+    for D in (64, 128):
+        for causal in (True, False):
+            q, k, v, do = make_inputs(1, 2, S, D, dtype, seed=31 * S + D)
+            say(f"edge dtype={dtype} S={S} D={D} causal={causal}")
+            got = gpu_fwd_bwd(q, k, v, do, 0.125, causal)
+            compare_all(dtype, got, q, k, v, do, 0.125, causal)
+
+
+def test_empty_problem(cuda):
+    for shape in ((0, 2, 16, 64), (1, 0, 16, 64), (1, 2, 0, 64)):
+        q = torch.empty(shape, dtype=torch.bfloat16, device=DEV)
+        say(f"empty {shape}")
+        o, lse = attn_fwd(q, q.clone(), q.clone(), 0.125, True)
+        dq, dk, dv = attn_bwd(q, q.clone(), q.clone(), o, q.clone(), lse, 0.125, True)
+        torch.cuda.synchronize()
+        assert o.shape == shape and dq.shape == shape and lse.shape == shape[:3]
+
+
+def sampled_heads(B, H):
+    return sorted({(0, 0), (B // 2, H // 2), (B - 1, H - 1)})
+
+
+@pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
+def test_workload_parity(cuda, w):
+    """Full-size run; every element of the sampled (batch, head) slices is compared."""
+    q, k, v, do = workload_inputs(w)
+    say(f"workload {w.name}")
+    got = gpu_fwd_bwd(q, k, v, do, w.scale, w.causal)
+    heads = sampled_heads(w.B, w.H) if w.B * w.H > 4 else [(b, h) for b in range(w.B) for h in range(w.H)]
+    sel = lambda t: torch.stack([t[b, h] for b, h in heads])[None]  # noqa: E731
+    qs, ks, vs, dos = (sel(t) for t in (q, k, v, do))
+    compare_all(w.dtype, tuple(sel(t) for t in got), qs, ks, vs, dos, w.scale, w.causal)
+    for t in got:
+        assert torch.isfinite(t.float()).all()
+
+
+def test_bwd_isolated_from_fwd(cuda):
+    """GPU backward fed the oracle's O (rounded to the storage dtype) and LSE."""
+    for dtype, S, D in (("f32", 128, 64), ("bf16", 512, 64), ("bf16", 256, 128)):
+        q, k, v, do = make_inputs(1, 2, S, D, dtype, seed=4242 + S)
+        scale = 1.0 / math.sqrt(D)
+        ro, rlse = orc.attn_fwd(q, k, v, scale, True)
+        td = torch.float32 if dtype == "f32" else torch.bfloat16
+        o = torch.tensor(ro, dtype=torch.float32).to(td).to(DEV)
+        lse = torch.tensor(rlse, dtype=torch.float32).to(DEV)
+        say(f"bwd-isolated dtype={dtype} S={S} D={D}")
+        dq, dk, dv = attn_bwd(q.to(DEV), k.to(DEV), v.to(DEV), o, do.to(DEV), lse, scale, True)
+        torch.cuda.synchronize()
+        rdq, rdk, rdv = orc.attn_bwd(q, k, v, do, scale, True)
+        for n, g, r in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
+            check_tensor(n, dtype, g.cpu(), r)
+
+
+def test_gpu_invariants(cuda):
+    """Closed forms and invariants checked directly on GPU outputs."""
+    w = WORKLOADS[1]
+    q, k, v, do = make_inputs(2, 3, 1024, 64, "bf16", seed=99)
+    say("invariants bf16 B2 H3 S1024 D64")
+    o, lse, dq, dk, dv = gpu_fwd_bwd(q, k, v, do, w.scale, True)
+    # query 0 sees only key 0: P = 1 exactly, so O_0 = V_0 bit for bit
+    assert torch.equal(o[:, :, 0], v[:, :, 0])
+    ref_lse0 = w.scale * (to64(q[:, :, 0]) * to64(k[:, :, 0])).sum(-1)
+    assert np.max(np.abs(to64(lse[:, :, 0]) - ref_lse0)) <= 1e-3
+    # sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i, relative to the size of the terms
+    dk64, dv64, do64 = to64(dk), to64(dv), to64(do)
+    assert np.linalg.norm(dk64.sum(2)) <= 1e-2 * np.linalg.norm(np.abs(dk64).sum(2))
+    assert np.linalg.norm(dv64.sum(2) - do64.sum(2)) <= 1e-2 * np.linalg.norm(do64.sum(2))
+    # Q = 0: O_i is the running mean of V_0..V_i, LSE_i = ln(i + 1)
+    z = torch.zeros_like(q)
+    say("invariants Q=0 prefix mean")
+    o0, lse0, *_ = gpu_fwd_bwd(z, k, v, do, w.scale, True)
+    prefix = np.cumsum(to64(v), axis=2) / np.arange(1, 1025)[None, None, :, None]
+    assert np.linalg.norm(to64(o0) - prefix) <= 1e-2 * np.linalg.norm(prefix)
+    assert np.max(np.abs(to64(lse0) - np.log(np.arange(1, 1025)))) <= 1e-3
+
+
+def test_deterministic(cuda):
+    """No atomics: two runs give bitwise identical outputs."""
+    w = WORKLOADS[1]
+    q, k, v, do = workload_inputs(w)
+    say("determinism gpt2-small")
+    a = gpu_fwd_bwd(q, k, v, do, w.scale, True)
+    b = gpu_fwd_bwd(q, k, v, do, w.scale, True)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_side_stream_matches_default(cuda):
+    q, k, v, do = (t.to(DEV) for t in make_inputs(2, 2, 384, 64, "bf16", seed=5))
+    say("side stream")
+    o1, l1 = attn_fwd(q, k, v, 0.125, True)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        o2, l2 = attn_fwd(q, k, v, 0.125, True)
+        g2 = attn_bwd(q, k, v, o2, do, l2, 0.125, True)
+    torch.cuda.current_stream().wait_stream(s)
+    g1 = attn_bwd(q, k, v, o1, do, l1, 0.125, True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    for x, y in zip(g1, g2):
+        assert torch.equal(x, y)
