@@ -1,0 +1,183 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused causal attention hot path on one MI355X.
+
+A step is one forward (O, LSE) plus one backward (dQ + D, then dK, dV) over the
+GPT-2-small attention workload, bf16, B=8 H=12 S=1024 D=64, causal, scale 1/8,
+with every input already resident in HBM.  Throughput is the counted causal
+FLOPs of the step (forward 2*B*H*S^2*D, backward 5*B*H*S^2*D) over the wall
+time of exactly --steps steps, bracketed by device synchronisations.
+
+The same timed region also records HIP events around each kernel on the
+stream the kernels run on; the slowest kernel's mean duration gives the
+roofline entry.  On rank 0 the float64 CPU oracle is then timed on a bounded
+sample of the same workload (whole (batch, head) slices) as a reported
+baseline.  Prints ONE JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "causal attention fwd+bwd TFLOP/s (bf16, 1 MI355X) at B8 H12 S1024 D64; % MFMA peak"
+DEFAULT_WORKLOAD = "gpt2_small_B8_H12_S1024_D64"
+# MI355X dense matrix-core peaks (TFLOP/s): 256 CUs x 2.4 GHz x FLOP/clock/CU
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+
+
+def kernel_flops(w):
+    """Algorithmic FLOPs per launch of each kernel: 2*D per contraction per
+    visible (query, key) pair, B*H*S^2/2 pairs when causal (B*H*S^2 if not).
+    forward: 2 contractions (Q K^T, P V); dq kernel: 3 (Q K^T, dO V^T, dS K);
+    dk/dv kernel: 4 (Q K^T, dO V^T, P^T dO, dS^T Q)."""
+    pairs = w.B * w.H * w.S * w.S * (0.5 if w.causal else 1.0)
+    per = 2.0 * w.D * pairs
+    return {"attn_fwd": 2 * per, "attn_bwd_dq": 3 * per, "attn_bwd_dkdv": 4 * per}
+
+
+def cpu_baseline(w, inputs, budget_s: float):
+    """Time the float64 oracle (as it stands) on whole (batch, head) slices of
+    the workload until about `budget_s` seconds have been spent."""
+    import oracle.attn_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    q, k, v, do = inputs
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+    done = 0
+    t0 = time.perf_counter()
+    for b, h in heads:
+        sl = lambda t: t[b:b + 1, h:h + 1]  # noqa: E731
+        orc.attn_fwd(sl(q), sl(k), sl(v), w.scale, w.causal)
+        orc.attn_bwd(sl(q), sl(k), sl(v), sl(do), w.scale, w.causal)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    fwd_f, bwd_f = w.counted_flops()
+    per_head = (fwd_f + bwd_f) / (w.B * w.H)
+    return {"value": round(per_head * done / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} of {w.B * w.H} (batch, head) slices of {w.name}, fwd+bwd in float64, "
+                      f"{dt:.1f} s wall"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the CPU-oracle baseline (0 disables it)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures the attention kernels on ONE GPU only; "
+              "multi-GPU runs (--gpus N > 1) are not part of it.", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2608_00029_amd import binding as bd
+    from paper_2608_00029_amd.workloads import BY_NAME, workload_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py: no HIP device visible", file=sys.stderr)
+        return 1
+    w = BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    cpu_inputs = workload_inputs(w)
+    q, k, v, do = (t.to(dev) for t in cpu_inputs)
+    o = torch.empty_like(q)
+    lse = torch.empty((w.B, w.H, w.S), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    ws = torch.empty((w.B * w.H * w.S,), dtype=torch.float32, device=dev)
+    dcode = bd.CATTN_BF16 if w.dtype == "bf16" else bd.CATTN_F32
+    L = bd.lib()
+    stream = torch.cuda.current_stream(dev)
+    sp = __import__("ctypes").c_void_p(stream.cuda_stream)
+    P = lambda t: t.data_ptr()  # noqa: E731
+    shape = (w.B, w.H, w.S, w.D, float(w.scale), int(w.causal), dcode, sp)
+
+    def fwd():
+        return L.cattn_attn_fwd(P(q), P(k), P(v), P(o), P(lse), *shape)
+
+    def bwd_dq():
+        return L.cattn_attn_bwd_dq(P(q), P(k), P(v), P(o), P(do), P(lse), P(dq), P(ws), *shape)
+
+    def bwd_dkdv():
+        return L.cattn_attn_bwd_dkdv(P(q), P(k), P(v), P(do), P(lse), P(ws), P(dk), P(dv), *shape)
+
+    kernels = [("attn_fwd", fwd), ("attn_bwd_dq", bwd_dq), ("attn_bwd_dkdv", bwd_dkdv)]
+    for _ in range(args.warmup):
+        for name, f in kernels:
+            st = f()
+            if st != 0:
+                raise RuntimeError(f"{name}: {bd.status_string(st)}: {bd.last_error_string()}")
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        e = ev[i]
+        e[0].record(stream)
+        for j, (_, f) in enumerate(kernels):
+            f()
+            e[j + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    per_kernel_ms = {name: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(args.steps)) / args.steps
+                     for j, (name, _) in enumerate(kernels)}
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    fwd_f, bwd_f = w.counted_flops()
+    tflops = (fwd_f + bwd_f) / (ms_per_step * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+
+    kf = kernel_flops(w)
+    dom = max(per_kernel_ms, key=per_kernel_ms.get)
+    achieved = kf[dom] / (per_kernel_ms[dom] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                "flops_per_launch": kf[dom], "mean_launch_us": round(per_kernel_ms[dom] * 1e3, 2)}
+
+    line = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic: seeded N(0,1) Q, K, V, dO rounded to bf16, inputs resident in HBM",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "S": w.S, "D": w.D, "causal": w.causal,
+                   "scale": w.scale, "parallelism": "single-gpu"},
+        "pct_mfma_peak": round(100.0 * tflops / peak, 2),
+        "kernels_us": {n: round(t * 1e3, 2) for n, t in per_kernel_ms.items()},
+        "roofline": roofline,
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(w, cpu_inputs, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

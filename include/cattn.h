@@ -111,6 +111,31 @@ cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
                             int B, int H, int S, int D,
                             float scale, int causal, int dtype, void* stream);
 
+/*
+ * The two phases of cattn_attn_bwd as separate calls, for callers that
+ * schedule or time them individually.  cattn_attn_bwd(...) is exactly
+ * cattn_attn_bwd_dq(...) followed by cattn_attn_bwd_dkdv(...) on one stream.
+ *
+ * cattn_attn_bwd_dq: the kernel that reduces over keys.  Writes dq and D =
+ *   rowsum(dO * O) (float [B, H, S]) into `workspace`.  Same argument rules as
+ *   cattn_attn_bwd for the arguments it takes.
+ * cattn_attn_bwd_dkdv: the kernel that reduces over queries.  Reads D from
+ *   `workspace`, which must hold what cattn_attn_bwd_dq wrote for the same
+ *   inputs (ordered before this call on `stream`, or otherwise complete).
+ *   Writes dk and dv.
+ */
+cattn_status cattn_attn_bwd_dq(const void* q, const void* k, const void* v,
+                               const void* o, const void* dout, const float* lse,
+                               void* dq, float* workspace,
+                               int B, int H, int S, int D,
+                               float scale, int causal, int dtype, void* stream);
+
+cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v,
+                                 const void* dout, const float* lse, const float* workspace,
+                                 void* dk, void* dv,
+                                 int B, int H, int S, int D,
+                                 float scale, int causal, int dtype, void* stream);
+
 /* Bytes of workspace cattn_attn_bwd needs: B * H * S * sizeof(float)
  * (0 for an empty or invalid shape). */
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);

@@ -21,8 +21,8 @@ _lib: Optional[ctypes.CDLL] = None
 CATTN_OK, CATTN_ERR_INVALID_ARG, CATTN_ERR_UNSUPPORTED, CATTN_ERR_HIP = 0, 1, 2, 3
 CATTN_F32, CATTN_BF16 = 0, 1
 
-EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_bwd_workspace_bytes", "cattn_status_string",
-            "cattn_last_error_string")
+EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_attn_bwd_dq", "cattn_attn_bwd_dkdv",
+            "cattn_bwd_workspace_bytes", "cattn_status_string", "cattn_last_error_string")
 
 
 class CattnError(RuntimeError):
@@ -48,6 +48,10 @@ def lib() -> ctypes.CDLL:
         L.cattn_attn_fwd.restype = i
         L.cattn_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
         L.cattn_attn_bwd.restype = i
+        L.cattn_attn_bwd_dq.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
+        L.cattn_attn_bwd_dq.restype = i
+        L.cattn_attn_bwd_dkdv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
+        L.cattn_attn_bwd_dkdv.restype = i
         L.cattn_bwd_workspace_bytes.argtypes = [i, i, i, i]
         L.cattn_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.cattn_status_string.argtypes = [i]
@@ -146,15 +150,57 @@ def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk
         _check(n, t, q.shape, q.dtype, q.device)
     if workspace is None:
         workspace = torch.empty((B * H * S,), dtype=torch.float32, device=q.device)
-    if workspace.dtype != torch.float32 or workspace.device != q.device or not workspace.is_contiguous() \
-            or workspace.numel() < B * H * S:
-        raise ValueError("workspace must be a contiguous float32 tensor of >= B*H*S elements on q's device")
+    _check_workspace(workspace, B * H * S, q.device)
     st = lib().cattn_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq), _ptr(dk),
                               _ptr(dv), _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)),
                               _dtype_code(q), _stream(q.device))
     if st != CATTN_OK:
         raise CattnError(st, "cattn_attn_bwd", last_error_string())
     return dq, dk, dv
+
+
+def attn_bwd_dq(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, workspace=None):
+    """First backward phase: dQ, and D = rowsum(dO * O) into `workspace` (returned)."""
+    B, H, S, D = q.shape
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    _check("lse", lse, (B, H, S), torch.float32, q.device)
+    dq = torch.empty_like(q) if dq is None else dq
+    _check("dq", dq, q.shape, q.dtype, q.device)
+    if workspace is None:
+        workspace = torch.empty((B * H * S,), dtype=torch.float32, device=q.device)
+    _check_workspace(workspace, B * H * S, q.device)
+    st = lib().cattn_attn_bwd_dq(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq),
+                                 _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)), _dtype_code(q),
+                                 _stream(q.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_attn_bwd_dq", last_error_string())
+    return dq, workspace
+
+
+def attn_bwd_dkdv(q, k, v, do, lse, workspace, scale: float, causal: bool = True, dk=None, dv=None):
+    """Second backward phase: dK, dV, reading D from `workspace` (written by attn_bwd_dq)."""
+    B, H, S, D = q.shape
+    for n, t in (("q", q), ("k", k), ("v", v), ("do", do)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    _check("lse", lse, (B, H, S), torch.float32, q.device)
+    _check_workspace(workspace, B * H * S, q.device)
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for n, t in (("dk", dk), ("dv", dv)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    st = lib().cattn_attn_bwd_dkdv(_ptr(q), _ptr(k), _ptr(v), _ptr(do), _ptr(lse), _ptr(workspace), _ptr(dk),
+                                   _ptr(dv), B, H, S, D, float(scale), int(bool(causal)), _dtype_code(q),
+                                   _stream(q.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_attn_bwd_dkdv", last_error_string())
+    return dk, dv
+
+
+def _check_workspace(ws, n, device):
+    if not isinstance(ws, torch.Tensor) or ws.dtype != torch.float32 or ws.device != device \
+            or not ws.is_contiguous() or ws.numel() < n:
+        raise ValueError("workspace must be a contiguous float32 tensor of >= B*H*S elements on q's device")
 
 
 def raw_fwd(q_ptr: int, k_ptr: int, v_ptr: int, o_ptr: int, lse_ptr: int, B: int, H: int, S: int, D: int,

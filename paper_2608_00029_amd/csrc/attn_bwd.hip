@@ -272,14 +272,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(const T* __restrict_
 }
 
 template <typename T, int D, bool CAUSAL>
-static hipError_t launch_bwd_t(const BwdArgs& a, hipStream_t st) {
+static hipError_t launch_bwd_t(const BwdArgs& a, int phase, hipStream_t st) {
   const float c = a.scale * kLog2e;
-  const int n_qtiles = (a.S + 127) / 128;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256), 0,
-                     st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.o, (const T*)a.dout, a.lse,
-                     (T*)a.dq, a.dvec, a.S, a.BH, n_qtiles, c, a.scale);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (phase != 2) {
+    const int n_qtiles = (a.S + 127) / 128;
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256),
+                       0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.o, (const T*)a.dout, a.lse,
+                       (T*)a.dq, a.dvec, a.S, a.BH, n_qtiles, c, a.scale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || phase == 1) return e;
+  }
   const int n_ktiles = (a.S + 127) / 128;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_ktiles)), dim3(256),
                      0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, a.lse, a.dvec,
@@ -288,13 +290,13 @@ static hipError_t launch_bwd_t(const BwdArgs& a, hipStream_t st) {
 }
 
 template <typename T, int D>
-static hipError_t launch_bwd_d(const BwdArgs& a, hipStream_t st) {
-  return a.causal ? launch_bwd_t<T, D, true>(a, st) : launch_bwd_t<T, D, false>(a, st);
+static hipError_t launch_bwd_d(const BwdArgs& a, int phase, hipStream_t st) {
+  return a.causal ? launch_bwd_t<T, D, true>(a, phase, st) : launch_bwd_t<T, D, false>(a, phase, st);
 }
 
-hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
-  if (a.bf16) return a.D == 64 ? launch_bwd_d<__bf16, 64>(a, st) : launch_bwd_d<__bf16, 128>(a, st);
-  return a.D == 64 ? launch_bwd_d<float, 64>(a, st) : launch_bwd_d<float, 128>(a, st);
+hipError_t launch_bwd(const BwdArgs& a, int phase, hipStream_t st) {
+  if (a.bf16) return a.D == 64 ? launch_bwd_d<__bf16, 64>(a, phase, st) : launch_bwd_d<__bf16, 128>(a, phase, st);
+  return a.D == 64 ? launch_bwd_d<float, 64>(a, phase, st) : launch_bwd_d<float, 128>(a, phase, st);
 }
 
 int64_t bwd_grid_blocks(int BH, int S) { return (int64_t)BH * ((S + 127) / 128); }

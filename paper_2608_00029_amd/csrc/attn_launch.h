@@ -38,7 +38,8 @@ struct BwdArgs {
 };
 
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
-hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
+// phase: 0 = dq kernel then dkdv kernel, 1 = dq kernel only, 2 = dkdv kernel only
+hipError_t launch_bwd(const BwdArgs& a, int phase, hipStream_t st);
 int64_t fwd_grid_blocks(int BH, int S);
 int64_t bwd_grid_blocks(int BH, int S);
 

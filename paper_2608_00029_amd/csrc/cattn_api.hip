@@ -82,33 +82,77 @@ cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v, void* o
   return hip_status(cattn::launch_fwd(a, (hipStream_t)stream));
 }
 
-cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
-                            const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H, int S,
-                            int D, float scale, int causal, int dtype, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation + launch shared by the three backward entry points.  `ins` and
+// `outs` list the buffers each phase reads and writes; the workspace is an
+// output of phases 0 and 1 and an input of phase 2.
+cattn_status bwd_common(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                        const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H, int S,
+                        int D, float scale, int causal, int dtype, void* stream, int phase) {
   g_last_error[0] = '\0';
   bool empty;
   cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
   if (st != CATTN_OK || empty) return st;
-  if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv || !workspace)
+  const bool need_o = phase != 2, need_dq = phase != 2, need_dkdv = phase != 1;
+  if (!q || !k || !v || !dout || !lse || !workspace || (need_o && !o) || (need_dq && !dq) ||
+      (need_dkdv && (!dk || !dv)))
     return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
   if (((uintptr_t)workspace & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "workspace must be 4-byte aligned");
   const size_t esz = dtype == CATTN_BF16 ? 2 : 4;
   const size_t n = (size_t)B * H * S * D, nrow = (size_t)B * H * S;
-  const Range ins[] = {range_of(q, n * esz), range_of(k, n * esz), range_of(v, n * esz), range_of(o, n * esz),
-                       range_of(dout, n * esz), range_of(lse, nrow * 4)};
-  const Range outs[] = {range_of(dq, n * esz), range_of(dk, n * esz), range_of(dv, n * esz),
-                        range_of(workspace, nrow * 4)};
-  for (const Range& out : outs)
-    for (const Range& in : ins)
-      if (overlap(out, in)) return fail(CATTN_ERR_INVALID_ARG, "an output or the workspace overlaps an input");
-  for (int i = 0; i < 4; ++i)
-    for (int j = i + 1; j < 4; ++j)
+  Range ins[7], outs[4];
+  int ni = 0, no = 0;
+  ins[ni++] = range_of(q, n * esz);
+  ins[ni++] = range_of(k, n * esz);
+  ins[ni++] = range_of(v, n * esz);
+  ins[ni++] = range_of(dout, n * esz);
+  ins[ni++] = range_of(lse, nrow * 4);
+  if (need_o) ins[ni++] = range_of(o, n * esz);
+  if (phase == 2) ins[ni++] = range_of(workspace, nrow * 4);
+  else outs[no++] = range_of(workspace, nrow * 4);
+  if (need_dq) outs[no++] = range_of(dq, n * esz);
+  if (need_dkdv) {
+    outs[no++] = range_of(dk, n * esz);
+    outs[no++] = range_of(dv, n * esz);
+  }
+  for (int i = 0; i < no; ++i)
+    for (int j = 0; j < ni; ++j)
+      if (overlap(outs[i], ins[j])) return fail(CATTN_ERR_INVALID_ARG, "an output or the workspace overlaps an input");
+  for (int i = 0; i < no; ++i)
+    for (int j = i + 1; j < no; ++j)
       if (overlap(outs[i], outs[j])) return fail(CATTN_ERR_INVALID_ARG, "outputs or workspace overlap each other");
 
   cattn::BwdArgs a{q, k, v, o, dout, lse, dq, dk, dv, workspace, B * H, S, D, scale, causal != 0,
                    dtype == CATTN_BF16};
   (void)hipGetLastError();
-  return hip_status(cattn::launch_bwd(a, (hipStream_t)stream));
+  return hip_status(cattn::launch_bwd(a, phase, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                            const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H, int S,
+                            int D, float scale, int causal, int dtype, void* stream) {
+  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, workspace, B, H, S, D, scale, causal, dtype, stream, 0);
+}
+
+cattn_status cattn_attn_bwd_dq(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                               const float* lse, void* dq, float* workspace, int B, int H, int S, int D,
+                               float scale, int causal, int dtype, void* stream) {
+  return bwd_common(q, k, v, o, dout, lse, dq, nullptr, nullptr, workspace, B, H, S, D, scale, causal, dtype,
+                    stream, 1);
+}
+
+cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout, const float* lse,
+                                 const float* workspace, void* dk, void* dv, int B, int H, int S, int D,
+                                 float scale, int causal, int dtype, void* stream) {
+  return bwd_common(q, k, v, nullptr, dout, lse, nullptr, dk, dv, const_cast<float*>(workspace), B, H, S, D,
+                    scale, causal, dtype, stream, 2);
 }
 
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D) {

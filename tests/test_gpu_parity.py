@@ -175,3 +175,19 @@ def test_side_stream_matches_default(cuda):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
     for x, y in zip(g1, g2):
         assert torch.equal(x, y)
+
+
+def test_bwd_phases_match_fused_call(cuda):
+    """cattn_attn_bwd_dq followed by cattn_attn_bwd_dkdv equals cattn_attn_bwd bit for bit."""
+    from paper_2608_00029_amd import attn_bwd_dkdv, attn_bwd_dq
+    for dtype, D in (("bf16", 64), ("f32", 128)):
+        q, k, v, do = (t.to(DEV) for t in make_inputs(1, 3, 320, D, dtype, seed=11))
+        say(f"bwd phases dtype={dtype} D={D}")
+        o, lse = attn_fwd(q, k, v, 0.125, True)
+        g = attn_bwd(q, k, v, o, do, lse, 0.125, True)
+        dq, ws = attn_bwd_dq(q, k, v, o, do, lse, 0.125, True)
+        dk, dv = attn_bwd_dkdv(q, k, v, do, lse, ws, 0.125, True)
+        torch.cuda.synchronize()
+        assert torch.equal(g[0], dq) and torch.equal(g[1], dk) and torch.equal(g[2], dv)
+        ref_d = (do.double() * o.double()).sum(-1).reshape(-1)
+        assert torch.allclose(ws.double(), ref_d, rtol=1e-5, atol=1e-4)
