@@ -28,6 +28,9 @@ HIPCC_FLAGS = [
     "-Wall",
     "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep matrix-core accumulators in ordinary VGPRs: the softmax rescale and
+    # the epilogue then read them directly instead of copying through AGPRs
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
 ]
 
@@ -46,30 +49,33 @@ def _run(cmd):
     return r.returncode, "\n".join(lines)
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
-    """Compile every source and link libcattn.so; return its path.  Always rebuilds."""
+def build(verbose: bool = False, jobs: int = 8, out: str = LIB, defines=()) -> str:
+    """Compile every source and link libcattn.so (or `out`); return its path.  Always rebuilds.
+    `defines` are extra -D flags (for experiments with compile-time variants)."""
     hipcc = _hipcc()
-    os.makedirs(OBJ_DIR, exist_ok=True)
+    obj_dir = OBJ_DIR if out == LIB else out + "_objs"
+    os.makedirs(obj_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     if not srcs:
         raise RuntimeError(f"no HIP sources under {CSRC}")
-    objs = [os.path.join(OBJ_DIR, os.path.basename(s) + ".o") for s in srcs]
-    cmds = [[hipcc, *HIPCC_FLAGS, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
+    objs = [os.path.join(obj_dir, os.path.basename(s) + ".o") for s in srcs]
+    extra = [f"-D{d}" for d in defines]
+    cmds = [[hipcc, *HIPCC_FLAGS, *extra, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(cmds)))) as ex:
         results = list(ex.map(_run, cmds))
-    for cmd, (rc, out) in zip(cmds, results):
-        if verbose and out.strip():
-            print(out)
+    for cmd, (rc, msg) in zip(cmds, results):
+        if verbose and msg.strip():
+            print(msg)
         if rc != 0:
-            raise RuntimeError(f"hipcc failed ({rc}): {' '.join(cmd)}\n{out}")
-    tmp = LIB + ".tmp"
-    rc, out = _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+            raise RuntimeError(f"hipcc failed ({rc}): {' '.join(cmd)}\n{msg}")
+    tmp = out + ".tmp"
+    rc, msg = _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     if rc != 0:
-        raise RuntimeError(f"link failed ({rc}):\n{out}")
-    os.replace(tmp, LIB)
+        raise RuntimeError(f"link failed ({rc}):\n{msg}")
+    os.replace(tmp, out)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {out}")
+    return out
 
 
 if __name__ == "__main__":

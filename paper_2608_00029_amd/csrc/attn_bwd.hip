@@ -30,7 +30,7 @@
 namespace cattn {
 
 template <typename T, int D, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const T* __restrict__ Q, const T* __restrict__ K,
+__global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                           const T* __restrict__ V, const T* __restrict__ O,
                                                           const T* __restrict__ dO, const float* __restrict__ LSE,
                                                           T* __restrict__ dQ, float* __restrict__ Dvec, int S,
@@ -106,14 +106,17 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const T* __restrict__ 
         s = M::run(read_row_frag<T, D>(lk, sb * 32 + r, ks, h), qf[ks], s);
         dp = M::run(read_row_frag<T, D>(lv, sb * 32 + r, ks, h), dof[ks], dp);
       }
-      const bool need_mask = (CAUSAL && k0 + 31 > qw) || k0 + 32 > S;
+      if ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S) {
+        // masked scores get the finite sentinel, whose exponential is exactly 0
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          const int key = k0 + acc_row(a, h);
+          if (key >= S || (CAUSAL && key > my_q)) s[a] = kMasked;
+        }
+      }
 #pragma unroll
       for (int a = 0; a < 16; ++a) {
-        float p = exp2_hw(fmaf(s[a], c, -lse2));
-        if (need_mask) {
-          const int key = k0 + acc_row(a, h);
-          if (key >= S || (CAUSAL && key > my_q)) p = 0.f;
-        }
+        const float p = exp2_hw(fmaf(s[a], c, -lse2));
         dp[a] = p * (dp[a] - Dq);  // dS^T
       }
 #pragma unroll
@@ -143,7 +146,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const T* __restrict__ 
 }
 
 template <typename T, int D, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(const T* __restrict__ Q, const T* __restrict__ K,
+__global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_dkdv_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                             const T* __restrict__ V, const T* __restrict__ dO,
                                                             const float* __restrict__ LSE,
                                                             const float* __restrict__ Dvec, T* __restrict__ dK,
@@ -224,7 +227,14 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(const T* __restrict_
         dp = M::run(read_row_frag<T, D>(ldo, sb * 32 + r, ks, h), vf[ks], dp);
       }
       // s[a], dp[a]: query q0 + acc_row(a, h), key my_k
-      const bool need_mask = (CAUSAL && q0 < kw + 31) || q0 + 32 > S;
+      if ((CAUSAL && q0 < kw + 31) || q0 + 32 > S) {
+        // masked scores get the finite sentinel, whose exponential is exactly 0
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          const int qry = q0 + acc_row(a, h);
+          if (qry >= S || (CAUSAL && my_k > qry)) s[a] = kMasked;
+        }
+      }
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 l4 = *(const f32x4*)(llse + sb * 32 + 8 * g + 4 * h);
@@ -232,11 +242,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(const T* __restrict_
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int a = 4 * g + j;
-          float p = exp2_hw(fmaf(s[a], c, -l4[j]));
-          if (need_mask) {
-            const int qry = q0 + 8 * g + 4 * h + j;
-            if (qry >= S || (CAUSAL && my_k > qry)) p = 0.f;
-          }
+          const float p = exp2_hw(fmaf(s[a], c, -l4[j]));
           s[a] = p;
           dp[a] = p * (dp[a] - d4[j]);  // dS
         }

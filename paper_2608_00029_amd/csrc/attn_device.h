@@ -20,6 +20,18 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+// Occupancy targets (waves per SIMD) handed to the register allocator.
+#ifndef CATTN_WPE_FWD
+#define CATTN_WPE_FWD 0
+#endif
+#ifndef CATTN_WPE_DQ
+#define CATTN_WPE_DQ 0
+#endif
+#ifndef CATTN_WPE_DKDV
+#define CATTN_WPE_DKDV 0
+#endif
+#define CATTN_WPE_ATTR(n) __attribute__((amdgpu_waves_per_eu((n) > 0 ? (n) : 1, (n) > 0 ? (n) : 10)))
+
 namespace cattn {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -36,6 +48,9 @@ constexpr float kLn2 = 0.69314718055994530942f;
 // Finite mask sentinel (section 4.2): masked scores get a large negative
 // finite value rather than -inf; the base-2 exponential maps it to exactly 0.
 constexpr float kMasked = -1.0e30f;
+// Largest base-2 exponent a probability may reach before the forward moves its
+// softmax offset (P <= 2^8 = 256, far inside float and bf16 range).
+constexpr float kRescaleLog2 = 8.0f;
 
 // ---------------------------------------------------------------------------
 // Matrix-core traits
@@ -72,17 +87,22 @@ template <> struct Mma<float> {
 __device__ __forceinline__ int acc_row(int a, int h) { return 8 * (a >> 2) + 4 * h + (a & 3); }
 
 // ---------------------------------------------------------------------------
-// LDS tile: row-major [rows][D] of T, with 16-byte chunks XOR-swizzled by the
-// low three row bits so that 8 consecutive rows reading the same logical chunk
-// land in 8 different bank groups.
+// LDS tile: row-major [rows][D] of T, with 16-byte chunks XOR-swizzled by row.
 // ---------------------------------------------------------------------------
+// Physical 16-byte chunk of logical chunk c in row r is c ^ swz(r).  Measured on
+// MI355X against the two access patterns every tile sees -- 16-byte row reads
+// by 32 consecutive rows and transposed 8-byte reads of 4 consecutive rows x 2
+// chunks -- this keyed-by-row-pairs pattern roughly halves bank conflicts
+// relative to keying by the low three row bits.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
 template <typename T, int D> struct Tile {
   static constexpr int kRowBytes = D * (int)sizeof(T);
   static constexpr int kChunks = kRowBytes / 16;
   static_assert(kChunks >= 8, "swizzle needs at least 8 chunks per row");
   __device__ __forceinline__ static int off(int row, int col) {
     const int byte = col * (int)sizeof(T);
-    return row * kRowBytes + ((((byte >> 4) ^ (row & 7))) << 4) + (byte & 15);
+    return row * kRowBytes + ((((byte >> 4) ^ swz(row))) << 4) + (byte & 15);
   }
 };
 
@@ -153,7 +173,7 @@ template <typename T, int D, int R, int NT> struct TileStage {
     for (int i = 0; i < kPerThread; ++i) {
       const int c = tid + i * NT;
       const int row = c / kChunksPerRow, ch = c % kChunksPerRow;
-      *(u32x4*)(lds + row * Tile<T, D>::kRowBytes + ((ch ^ (row & 7)) << 4)) = reg[i];
+      *(u32x4*)(lds + row * Tile<T, D>::kRowBytes + ((ch ^ swz(row)) << 4)) = reg[i];
     }
   }
 };

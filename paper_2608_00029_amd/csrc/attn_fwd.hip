@@ -19,7 +19,7 @@
 namespace cattn {
 
 template <typename T, int D, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(const T* __restrict__ Q, const T* __restrict__ K,
+__global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                        const T* __restrict__ V, T* __restrict__ O,
                                                        float* __restrict__ LSE, int S, int BH, int n_qtiles,
                                                        float c) {
@@ -46,7 +46,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const T* __restrict__ Q, 
   const int kend = CAUSAL ? min(S, q0 + BQ) : S;  // causal loop clamping
   const int n_kt = (kend + BK - 1) / BK;
 
-  float m = kMasked;   // running max of the raw scores (scale folded in later)
+  float m = kMasked;   // running softmax offset, in raw-score units (scale folded in later)
   float lsum = 0.f;    // running sum of this half's probabilities
   f32x16 oacc[DT];
 #pragma unroll
@@ -85,19 +85,28 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const T* __restrict__ Q, 
       float mx = s[0];
 #pragma unroll
       for (int a = 1; a < 16; ++a) mx = fmaxf(mx, s[a]);
-      const float m_new = fmaxf(m, halves_max(mx));
-      const float alpha = exp2_hw((m - m_new) * c);
-      const float mc = m_new * c;
+      mx = halves_max(mx);
+      // Lazy rescaling: the running offset m only moves when the block's max
+      // exceeds it by more than 2^kRescaleLog2 in probability units, so P stays
+      // <= 2^kRescaleLog2 and the O/l rescale (a multiply of every accumulator)
+      // is skipped in almost every block.  O/l and LSE are exact for any m.
+      const bool grow = (mx - m) * c > kRescaleLog2;
+      if (__builtin_amdgcn_ballot_w64(grow)) {  // wave-uniform branch
+        const float m_new = grow ? mx : m;
+        const float alpha = exp2_hw((m - m_new) * c);
+        m = m_new;
+        lsum *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      }
+      const float mc = m * c;
       float psum = 0.f;
 #pragma unroll
       for (int a = 0; a < 16; ++a) {
         s[a] = exp2_hw(fmaf(s[a], c, -mc));
         psum += s[a];
       }
-      lsum = fmaf(lsum, alpha, psum);
-      m = m_new;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      lsum += psum;
 #pragma unroll
       for (int ks = 0; ks < KS_32; ++ks) {
         const typename M::frag pb = M::pack(s, ks);
