@@ -121,7 +121,7 @@ def main() -> int:
     o = torch.empty_like(q)
     lse = torch.empty((w.B, w.H, w.S), dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    ws = torch.empty((w.B * w.H * w.S,), dtype=torch.float32, device=dev)
+    ws = torch.empty((bd.workspace_bytes(w.B, w.H, w.S, w.D) // 4,), dtype=torch.float32, device=dev)
     dcode = bd.CATTN_BF16 if w.dtype == "bf16" else bd.CATTN_F32
     L = bd.lib()
     stream = torch.cuda.current_stream(dev)

@@ -133,7 +133,8 @@ def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk
              workspace=None):
     """dQ, dK, dV of attention for upstream gradient `do`, given the forward's O and LSE.
 
-    `workspace` (float32, >= B*H*S elements) receives D = rowsum(dO * O).
+    `workspace` (float32, >= workspace_bytes(B, H, S, D) / 4 elements) receives D = rowsum(dO * O)
+    and LSE * log2(e), each [B*H, S rounded up to 32] with zero padding rows.
     """
     if q.dim() != 4:
         raise ValueError("q must be [B, H, S, D]")
@@ -148,9 +149,10 @@ def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk
     dv = torch.empty_like(q) if dv is None else dv
     for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
         _check(n, t, q.shape, q.dtype, q.device)
+    nws = workspace_bytes(B, H, S, D) // 4
     if workspace is None:
-        workspace = torch.empty((B * H * S,), dtype=torch.float32, device=q.device)
-    _check_workspace(workspace, B * H * S, q.device)
+        workspace = torch.empty((nws,), dtype=torch.float32, device=q.device)
+    _check_workspace(workspace, nws, q.device)
     st = lib().cattn_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq), _ptr(dk),
                               _ptr(dv), _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)),
                               _dtype_code(q), _stream(q.device))
@@ -167,9 +169,10 @@ def attn_bwd_dq(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None,
     _check("lse", lse, (B, H, S), torch.float32, q.device)
     dq = torch.empty_like(q) if dq is None else dq
     _check("dq", dq, q.shape, q.dtype, q.device)
+    nws = workspace_bytes(B, H, S, D) // 4
     if workspace is None:
-        workspace = torch.empty((B * H * S,), dtype=torch.float32, device=q.device)
-    _check_workspace(workspace, B * H * S, q.device)
+        workspace = torch.empty((nws,), dtype=torch.float32, device=q.device)
+    _check_workspace(workspace, nws, q.device)
     st = lib().cattn_attn_bwd_dq(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq),
                                  _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)), _dtype_code(q),
                                  _stream(q.device))
@@ -184,7 +187,7 @@ def attn_bwd_dkdv(q, k, v, do, lse, workspace, scale: float, causal: bool = True
     for n, t in (("q", q), ("k", k), ("v", v), ("do", do)):
         _check(n, t, q.shape, q.dtype, q.device)
     _check("lse", lse, (B, H, S), torch.float32, q.device)
-    _check_workspace(workspace, B * H * S, q.device)
+    _check_workspace(workspace, workspace_bytes(B, H, S, D) // 4, q.device)
     dk = torch.empty_like(q) if dk is None else dk
     dv = torch.empty_like(q) if dv is None else dv
     for n, t in (("dk", dk), ("dv", dv)):
@@ -200,7 +203,8 @@ def attn_bwd_dkdv(q, k, v, do, lse, workspace, scale: float, causal: bool = True
 def _check_workspace(ws, n, device):
     if not isinstance(ws, torch.Tensor) or ws.dtype != torch.float32 or ws.device != device \
             or not ws.is_contiguous() or ws.numel() < n:
-        raise ValueError("workspace must be a contiguous float32 tensor of >= B*H*S elements on q's device")
+        raise ValueError("workspace must be a contiguous float32 tensor of >= cattn_bwd_workspace_bytes / 4 "
+                         "elements on q's device")
 
 
 def raw_fwd(q_ptr: int, k_ptr: int, v_ptr: int, o_ptr: int, lse_ptr: int, B: int, H: int, S: int, D: int,

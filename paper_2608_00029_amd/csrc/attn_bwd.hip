@@ -41,7 +41,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   constexpr int TILE = BK * D * (int)sizeof(T);
   __shared__ __attribute__((aligned(16))) char smem[2 * 2 * TILE];  // [buffer][K, V]
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   int bh, qt;
   tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
   const int64_t base = (int64_t)bh * S * D;
@@ -70,9 +71,11 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   }
   const float Dq = halves_sum(dpart);
   float lse2 = 0.f;
-  if (my_q < S) {
-    lse2 = LSE[(int64_t)bh * S + my_q] * kLog2e;
-    if (h == 0) Dvec[(int64_t)bh * S + my_q] = Dq;
+  if (my_q < S) lse2 = LSE[(int64_t)bh * S + my_q] * kLog2e;
+  const int Sp = ws_rows(S);
+  if (h == 0 && my_q < Sp) {  // workspace: D, then LSE * log2(e); padding rows are zero
+    Dvec[(int64_t)bh * Sp + my_q] = my_q < S ? Dq : 0.f;
+    Dvec[((int64_t)BH + bh) * Sp + my_q] = lse2;
   }
 
   const int kend = CAUSAL ? min(S, q0 + BQ) : S;
@@ -160,14 +163,15 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
   constexpr int BUF = 2 * TILE + 2 * VEC;     // Q, dO, LSE*log2e, D
   __shared__ __attribute__((aligned(16))) char smem[2 * BUF];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   int bh, kt;
   tile_of_block(blockIdx.x, BH, n_ktiles, false, bh, kt);
   const int64_t base = (int64_t)bh * S * D;
   const T* Qb = Q + base;
   const T* dOb = dO + base;
   const float* Lb = LSE + (int64_t)bh * S;
-  const float* Db = Dvec + (int64_t)bh * S;
+  const float* Db = Dvec + (int64_t)bh * ws_rows(S);
 
   const int k0 = kt * BKV, kw = k0 + 32 * w, my_k = kw + r;
   typename M::frag kf[KS_D], vf[KS_D];
@@ -284,13 +288,13 @@ static hipError_t launch_bwd_t(const BwdArgs& a, int phase, hipStream_t st) {
     const int n_qtiles = (a.S + 127) / 128;
     hipLaunchKernelGGL((attn_bwd_dq_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256),
                        0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.o, (const T*)a.dout, a.lse,
-                       (T*)a.dq, a.dvec, a.S, a.BH, n_qtiles, c, a.scale);
+                       (T*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || phase == 1) return e;
   }
   const int n_ktiles = (a.S + 127) / 128;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_ktiles)), dim3(256),
-                     0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, a.lse, a.dvec,
+                     0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, a.lse, a.ws,
                      (T*)a.dk, (T*)a.dv, a.S, a.BH, n_ktiles, c, a.scale);
   return hipGetLastError();
 }
@@ -301,7 +305,7 @@ static hipError_t launch_bwd_d(const BwdArgs& a, int phase, hipStream_t st) {
 }
 
 hipError_t launch_bwd(const BwdArgs& a, int phase, hipStream_t st) {
-  if (a.bf16) return a.D == 64 ? launch_bwd_d<__bf16, 64>(a, phase, st) : launch_bwd_d<__bf16, 128>(a, phase, st);
+  if (a.bf16) return launch_bwd_bf16(a, phase, st);
   return a.D == 64 ? launch_bwd_d<float, 64>(a, phase, st) : launch_bwd_d<float, 128>(a, phase, st);
 }
 

@@ -31,7 +31,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_ke
   constexpr int TILE = BK * D * (int)sizeof(T);
   __shared__ __attribute__((aligned(16))) char smem[2 * 2 * TILE];  // [buffer][K, V]
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   int bh, qt;
   tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
   const int64_t base = (int64_t)bh * S * D;
@@ -154,7 +155,7 @@ static hipError_t launch_fwd_d(const FwdArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st) {
-  if (a.bf16) return a.D == 64 ? launch_fwd_d<__bf16, 64>(a, st) : launch_fwd_d<__bf16, 128>(a, st);
+  if (a.bf16) return launch_fwd_bf16(a, st);
   return a.D == 64 ? launch_fwd_d<float, 64>(a, st) : launch_fwd_d<float, 128>(a, st);
 }
 

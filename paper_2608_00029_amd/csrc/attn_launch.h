@@ -8,6 +8,11 @@
 
 namespace cattn {
 
+// Rows per (batch, head) of each backward workspace array: S padded to a
+// multiple of 32 (padding rows hold zeros), so that 32-row tiles of it can be
+// copied whole.
+__host__ __device__ inline int ws_rows(int S) { return (S + 31) / 32 * 32; }
+
 struct FwdArgs {
   const void* q;
   const void* k;
@@ -30,7 +35,7 @@ struct BwdArgs {
   void* dq;
   void* dk;
   void* dv;
-  float* dvec;  // D = rowsum(dO * O), [BH, S] float
+  float* ws;  // workspace: D = rowsum(dO * O) then LSE * log2(e), each [BH, ws_rows(S)] float
   int BH, S, D;
   float scale;
   bool causal;
@@ -40,6 +45,9 @@ struct BwdArgs {
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
 // phase: 0 = dq kernel then dkdv kernel, 1 = dq kernel only, 2 = dkdv kernel only
 hipError_t launch_bwd(const BwdArgs& a, int phase, hipStream_t st);
+// bf16 kernels (attn_bf16.hip); launch_fwd / launch_bwd route bf16 calls here
+hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_bf16(const BwdArgs& a, int phase, hipStream_t st);
 int64_t fwd_grid_blocks(int BH, int S);
 int64_t bwd_grid_blocks(int BH, int S);
 

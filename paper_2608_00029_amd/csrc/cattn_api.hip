@@ -10,6 +10,8 @@
 #include "../../include/cattn.h"
 #include "attn_launch.h"
 
+extern "C" size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);
+
 namespace {
 
 thread_local char g_last_error[256] = "";
@@ -103,6 +105,7 @@ cattn_status bwd_common(const void* q, const void* k, const void* v, const void*
   if (((uintptr_t)workspace & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "workspace must be 4-byte aligned");
   const size_t esz = dtype == CATTN_BF16 ? 2 : 4;
   const size_t n = (size_t)B * H * S * D, nrow = (size_t)B * H * S;
+  const size_t wsb = cattn_bwd_workspace_bytes(B, H, S, D);
   Range ins[7], outs[4];
   int ni = 0, no = 0;
   ins[ni++] = range_of(q, n * esz);
@@ -111,8 +114,8 @@ cattn_status bwd_common(const void* q, const void* k, const void* v, const void*
   ins[ni++] = range_of(dout, n * esz);
   ins[ni++] = range_of(lse, nrow * 4);
   if (need_o) ins[ni++] = range_of(o, n * esz);
-  if (phase == 2) ins[ni++] = range_of(workspace, nrow * 4);
-  else outs[no++] = range_of(workspace, nrow * 4);
+  if (phase == 2) ins[ni++] = range_of(workspace, wsb);
+  else outs[no++] = range_of(workspace, wsb);
   if (need_dq) outs[no++] = range_of(dq, n * esz);
   if (need_dkdv) {
     outs[no++] = range_of(dk, n * esz);
@@ -157,7 +160,7 @@ cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
 
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D) {
   if (B <= 0 || H <= 0 || S <= 0 || D <= 0) return 0;
-  return (size_t)B * H * S * sizeof(float);
+  return 2 * (size_t)B * H * (size_t)cattn::ws_rows(S) * sizeof(float);
 }
 
 const char* cattn_status_string(int status) {

@@ -46,7 +46,8 @@ def test_status_strings(lib):
 
 
 def test_workspace_bytes(lib):
-    assert b.workspace_bytes(8, 12, 1024, 64) == 8 * 12 * 1024 * 4
+    assert b.workspace_bytes(8, 12, 1024, 64) == 2 * 8 * 12 * 1024 * 4
+    assert b.workspace_bytes(1, 2, 33, 64) == 2 * 1 * 2 * 64 * 4  # rows padded to a multiple of 32
     assert b.workspace_bytes(0, 12, 1024, 64) == 0
     assert b.workspace_bytes(-1, 12, 1024, 64) == 0
 
