@@ -101,8 +101,10 @@ cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v,
  *   dq,dk,dv : out, [B, H, S, D] `dtype` (must not overlap any input, each
  *              other, or the workspace)
  *   workspace: scratch of at least cattn_bwd_workspace_bytes(B, H, S, D)
- *              bytes, 4-byte aligned; on return it holds D as float [B, H, S].
- *              Its prior contents are ignored.
+ *              bytes, 4-byte aligned.  Its prior contents are ignored.  On
+ *              return it holds, as float [B*H][2][Sp] with Sp = S rounded up
+ *              to a multiple of 32: row 0 of head bh is D = rowsum(dO * O),
+ *              row 1 is LSE * log2(e); entries S..Sp-1 of both rows are 0.
  *   scale, causal: the values the forward was called with.
  */
 cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
@@ -116,11 +118,12 @@ cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
  * schedule or time them individually.  cattn_attn_bwd(...) is exactly
  * cattn_attn_bwd_dq(...) followed by cattn_attn_bwd_dkdv(...) on one stream.
  *
- * cattn_attn_bwd_dq: the kernel that reduces over keys.  Writes dq and D =
- *   rowsum(dO * O) (float [B, H, S]) into `workspace`.  Same argument rules as
- *   cattn_attn_bwd for the arguments it takes.
- * cattn_attn_bwd_dkdv: the kernel that reduces over queries.  Reads D from
- *   `workspace`, which must hold what cattn_attn_bwd_dq wrote for the same
+ * cattn_attn_bwd_dq: the kernel that reduces over keys.  Writes dq, and D =
+ *   rowsum(dO * O) and LSE * log2(e) into `workspace` in the layout given
+ *   above.  Same argument rules as cattn_attn_bwd for the arguments it takes.
+ * cattn_attn_bwd_dkdv: the kernel that reduces over queries.  Reads D and
+ *   LSE * log2(e) from `workspace` (bf16: both; float32: D, LSE from `lse`),
+ *   which must hold what cattn_attn_bwd_dq wrote for the same
  *   inputs (ordered before this call on `stream`, or otherwise complete).
  *   Writes dk and dv.
  */
@@ -136,8 +139,8 @@ cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v,
                                  int B, int H, int S, int D,
                                  float scale, int causal, int dtype, void* stream);
 
-/* Bytes of workspace cattn_attn_bwd needs: B * H * S * sizeof(float)
- * (0 for an empty or invalid shape). */
+/* Bytes of workspace cattn_attn_bwd needs: 2 * B * H * Sp * sizeof(float),
+ * Sp = S rounded up to a multiple of 32 (0 for an empty or invalid shape). */
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);
 
 /* Static, NUL-terminated name of a status code ("unknown status" otherwise). */

@@ -1,16 +1,20 @@
 // bf16 attention kernels for gfx950: forward, dQ and dK/dV (section 4.2 of the
-// Nova paper), organised around memory latency on CDNA4.
+// Nova paper), organised around memory latency and vector-ALU issue on CDNA4.
 //
 // Differences from the generic kernels (attn_fwd.hip, attn_bwd.hip, used for
 // float32):
 //  * Streamed operands move in tiles of 32 rows, HBM -> LDS with
 //    global_load_lds_dwordx4 (no staging registers, no ds_write), through a
-//    ring of Ring<D>::NBUF buffers.  The copy of tile t + AHEAD is issued at
-//    the top of tile t, so about AHEAD tiles of compute cover the latency of
-//    each copy; the wait at the top of tile t asks only for tile t+1 (newer
-//    copies stay in flight), then one barrier publishes it.  Rows past the
-//    end of the sequence are loaded from the last valid row (finite values)
-//    and masked in the kernel.
+//    ring of NB buffers.  The copy of tile t + NB - 1 is issued at the top of
+//    tile t, so several tiles of compute cover the latency of each copy; the
+//    wait at the top of tile t asks only for the tiles it is about to read
+//    (newer copies stay in flight), then one barrier publishes them.  Rows
+//    past the end of the sequence are loaded from the last valid row (finite
+//    values) and masked in the kernel.
+//  * The copies take a wave-uniform base address in scalar registers plus a
+//    per-lane 32-bit offset fixed for the whole kernel, and every loop is
+//    unrolled by the ring depth so that each LDS read names its buffer with an
+//    immediate offset: no per-iteration vector address arithmetic.
 //  * A 32-row tile is one sub-block of the matrix-core contractions.  Each
 //    wave walks its own range of sub-blocks; operands of sub-block j+1 are
 //    read from LDS (tile j+1 is always resident) while sub-block j computes.
@@ -19,6 +23,8 @@
 //    softmax of S(j).
 //  * Only the sub-block of a wave that straddles the causal diagonal (and the
 //    ragged last one) is masked; every other sub-block is branch-free.
+#include <utility>
+
 #include "attn_device.h"
 #include "attn_launch.h"
 
@@ -26,16 +32,35 @@ namespace cattn {
 
 typedef __bf16 bf16;
 typedef Mma<bf16> MB;
+template <int N> using IC = std::integral_constant<int, N>;
 
-#ifndef CATTN_TRACE
-#define CATTN_TRACE(slot)
+// Ring depths (buffers of 32-row tiles).  The forward at D = 64 runs two key
+// parts per workgroup, each with its own ring.
+#ifndef CATTN_FWD_NB64
+#define CATTN_FWD_NB64 3
+#endif
+#ifndef CATTN_FWD_NB128
+#define CATTN_FWD_NB128 4
+#endif
+#ifndef CATTN_BWD_NB64
+#define CATTN_BWD_NB64 6
+#endif
+#ifndef CATTN_BWD_NB128
+#define CATTN_BWD_NB128 4
 #endif
 
-// Ring geometry for 32-row tiles of D bf16 columns.
-template <int D> struct Ring {
-  static constexpr int NBUF = D == 64 ? 6 : 4;
-  static constexpr int AHEAD = NBUF - 1;                  // copy distance, in tiles
-  static constexpr int TILE = 32 * D * 2;                 // bytes of one tensor's tile
+// f(IC<0>{}), f(IC<1>{}), ..., f(IC<N-1>{}), in order.
+template <typename F, int... I>
+__device__ __forceinline__ void unroll_each(F& f, std::integer_sequence<int, I...>) {
+  (f(IC<I>{}), ...);
+}
+template <int N, typename F> __device__ __forceinline__ void unroll(F&& f) {
+  unroll_each(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int D> struct TileGeom {
+  static constexpr int TILE = 32 * D * 2;                 // bytes of one tensor's 32-row tile
+  static constexpr int CPR = D * 2 / 16;                  // 16-byte chunks per row
   static constexpr int DMA_PER_TENSOR = TILE / 16 / 256;  // copy instructions per thread
 };
 
@@ -81,33 +106,63 @@ __device__ __forceinline__ void tile_barrier(int n) {
   asm volatile("s_barrier" ::: "memory");
 }
 
-// One 16-byte HBM -> LDS copy per active lane.  The LDS destination (M0) is
-// wave-uniform; lane i's bytes land at M0 + 16 * i.  Issued as inline assembly
-// so that the compiler does not treat every later LDS read as aliasing the
-// copy in flight (it would then wait for the copy before each read);
-// completion is awaited explicitly (wait_vm) before the barrier that
-// publishes a tile.
-__device__ __forceinline__ void dma16(const void* src, const char* lds_wave_base) {
-  const unsigned dst = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)lds_wave_base);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(dst), "v"(src) : "memory", "m0");
+// Byte address of an LDS location (the value M0 takes).
+__device__ __forceinline__ unsigned lds_addr(const char* p) {
+  return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
 }
 
-// HBM -> LDS copy of a 32 x D bf16 tile (rows row0.. of g, row stride D).  The
-// chunk a lane deposits at physical position p of the tile is logical chunk
-// p ^ swz(row), so the LDS image has the swizzled layout Tile<> reads.  Rows
-// >= nrows are clamped to nrows - 1.
-template <int D>
-__device__ __forceinline__ void dma_tile(const bf16* g, int row0, int nrows, char* lds, int tid) {
-  constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-#pragma unroll
-  for (int i = 0; i < Ring<D>::DMA_PER_TENSOR; ++i) {
-    const int p = i * 256 + w * 64 + lane;
-    const int row = p / CPR, lc = (p % CPR) ^ swz(row);
-    const int grow = min(row0 + row, nrows - 1);
-    dma16(g + (int64_t)grow * D + lc * 8, lds + (i * 256 + w * 64) * 16);
-  }
+// One 16-byte HBM -> LDS copy per active lane: lane i copies the 16 bytes at
+// sbase + voff (sbase wave-uniform, in scalar registers) to LDS byte address
+// lds + 16 * i.  Issued as inline assembly so that the compiler does not treat
+// every later LDS read as aliasing the copy in flight (it would then wait for
+// the copy before each read); completion is awaited explicitly (wait_vm /
+// tile_barrier) before the barrier that publishes a tile.
+// M0 is a reserved register to the compiler, which warns about the clobber;
+// the clobber is what keeps it from assuming M0 survives the statement.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* sbase, unsigned voff, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
+               : "memory", "m0");
 }
+#pragma clang diagnostic pop
+
+// HBM -> LDS copy of 32-row tiles of a row-major [S][D] bf16 tensor.  The
+// chunk a lane deposits at physical position p of the tile is logical chunk
+// p ^ swz(row), so the LDS image has the swizzled layout Tile<> reads.  The
+// per-lane source offsets inside a tile are fixed for the kernel; only the
+// ragged last tile (rows >= nrows are read from row nrows - 1) recomputes them.
+template <int D> struct TileCopy {
+  typedef TileGeom<D> G;
+  unsigned voff[G::DMA_PER_TENSOR];
+  int w, lane;
+  __device__ __forceinline__ void init(int w_, int lane_) {
+    w = w_;
+    lane = lane_;
+#pragma unroll
+    for (int i = 0; i < G::DMA_PER_TENSOR; ++i) {
+      const int p = i * 256 + w * 64 + lane;
+      const int row = p / G::CPR;
+      voff[i] = (unsigned)(row * D * 2 + (((p % G::CPR) ^ swz(row)) << 4));
+    }
+  }
+  __device__ __forceinline__ void copy(const bf16* g, int row0, int nrows, char* lds) const {
+    const bf16* src = g + (int64_t)row0 * D;
+    const unsigned dst = lds_addr(lds) + w * 64 * 16;
+    if (row0 + 32 <= nrows) {
+#pragma unroll
+      for (int i = 0; i < G::DMA_PER_TENSOR; ++i) dma16(src, voff[i], dst + i * 256 * 16);
+    } else {
+#pragma unroll
+      for (int i = 0; i < G::DMA_PER_TENSOR; ++i) {
+        const int p = i * 256 + w * 64 + lane;
+        const int row = p / G::CPR, lc = (p % G::CPR) ^ swz(row);
+        const int src_row = min(row, nrows - 1 - row0);
+        dma16(src, (unsigned)(src_row * D * 2 + lc * 16), dst + i * 256 * 16);
+      }
+    }
+  }
+};
 
 // Row-major A-operand fragments of the 32 rows of a tile.
 template <int D>
@@ -125,6 +180,13 @@ __device__ __forceinline__ void read_trans(const char* lds, int lane, MB::frag (
     for (int dt = 0; dt < D / 32; ++dt) f[s][dt] = TransRead<bf16, D>::read(lds, 0, s, dt * 32, lane);
 }
 
+// Flip the sign of every element of a bf16 fragment.
+__device__ __forceinline__ MB::frag negated(MB::frag f) {
+  u32x4 u = __builtin_bit_cast(u32x4, f);
+  u ^= 0x80008000u;
+  return __builtin_bit_cast(MB::frag, u);
+}
+
 // Copies issued after tile t+1 and still allowed in flight at the top of
 // tile t, for a ring running AHEAD tiles ahead over n tiles.
 __device__ __forceinline__ int later_tiles(int t, int n, int ahead) {
@@ -132,46 +194,97 @@ __device__ __forceinline__ int later_tiles(int t, int n, int ahead) {
   return k > 0 ? k : 0;
 }
 
+// The forward keeps a softmax offset that moves only when a block's partial
+// probability sum exceeds this bound (or is not finite).  Probabilities are
+// then at most 2^32 (offset at most 32 below the running max, base 2), far
+// inside float and bf16 range even summed over 2^24 keys; O/l and LSE are
+// exact for any offset.
+constexpr float kSumMax = 4294967296.0f;
+
 // ---------------------------------------------------------------------------
 // Forward
+//
+// A workgroup owns 32*QG queries of one (batch, head), QG = 4/SPLIT query
+// groups of 32 (one per wave), and splits the keys it must visit into SPLIT
+// consecutive parts: wave w takes query group w % QG and key part w / QG.
+// Each part streams its own ring of K/V tiles, so the sequential chain of a
+// wave is 1/SPLIT of the key range (the critical path of the causal grid is
+// its heaviest query tile).  With SPLIT = 2 the two partial results of a
+// query group -- (O, running offset, running sum) -- merge lane to lane
+// through LDS at the end with the usual rescale-by-offset-difference rule.
+//
+// Online softmax in base 2 with a lazily moved offset: the exponentials of a
+// block are taken against the current offset m and summed in float; only
+// when some lane's sum leaves [0, kSumMax] (a score far above m, or the first
+// block, where m is the mask value) does the wave take the rare path that
+// computes the block max, moves m, rescales O and the running sum, and redoes
+// the block.  No per-block max is computed on the common path.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, int SPLIT, int NB>
 __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                             const bf16* __restrict__ V, bf16* __restrict__ O,
                                                             float* __restrict__ LSE, int S, int BH, int n_qtiles,
                                                             float c) {
-  typedef Ring<D> RG;
-  constexpr int BQ = 128, NB = RG::NBUF, AH = RG::AHEAD, TILE = RG::TILE;
+  typedef TileGeom<D> G;
+  constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
+  constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
-  constexpr int PER_TILE = 2 * RG::DMA_PER_TENSOR;
-  __shared__ __attribute__((aligned(16))) char smem[NB * 2 * TILE];  // [buffer][K, V]
+  constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR;
+  __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * SET];  // [part][slot][K, V]
+  static_assert(SPLIT == 1 || 2 * 64 * (2 * DT * 16 + 2) * 4 <= SPLIT * NB * SET, "merge area");
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
+  const int qg = w % QG, part = w / QG;
   int bh, qt;
   tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
   const int64_t base = (int64_t)bh * S * D;
   const bf16* Kb = K + base;
   const bf16* Vb = V + base;
 
-  const int q0 = qt * BQ, qw = q0 + 32 * w, my_q = qw + r;
-  const int kend = CAUSAL ? min(S, q0 + BQ) : S;  // causal loop clamping (workgroup)
-  const int n = (kend + 31) / 32;                  // 32-key tiles the workgroup visits
+  const int q0 = qt * BQ, qw = q0 + 32 * qg, my_q = qw + r;
+  const int kend = CAUSAL ? min(S, q0 + BQ) : S;   // causal loop clamping (workgroup)
+  const int n = (kend + 31) / 32;                   // 32-key tiles of the workgroup
+  const int L = (n + SPLIT - 1) / SPLIT;            // tiles per part (the last may be short)
   const int kend_w = qw >= S ? 0 : (CAUSAL ? min(S, qw + 32) : S);
-  const int nsb = (kend_w + 31) / 32;              // of which this wave uses the first nsb
+  const int nsb = (kend_w + 31) / 32;               // tiles this wave's queries need
+  const int tb = part * L;                          // this wave's tiles: [tb, te)
+  const int te = min(nsb, min(n, tb + L));
+  const int cnt = te > tb ? te - tb : 0;
 
-  auto buf = [&](int t) { return smem + (t % NB) * 2 * TILE; };
-  auto dma = [&](int t) {
-    dma_tile<D>(Kb, t * 32, S, buf(t), tid);
-    dma_tile<D>(Vb, t * 32, S, buf(t) + TILE, tid);
+  TileCopy<D> tc;
+  tc.init(w, lane);
+  const char* ring = smem + part * NB * SET;  // this wave's part
+  auto dma = [&](int i, auto slc) {  // iteration i's tile of every part, into ring slot slc
+    constexpr int sl = decltype(slc)::value;
+#pragma unroll
+    for (int p = 0; p < SPLIT; ++p) {
+      const int t = p * L + i;
+      if (i < L && t < n) {
+        char* dst = smem + (p * NB + sl) * SET;
+        tc.copy(Kb, t * 32, S, dst);
+        tc.copy(Vb, t * 32, S, dst + TILE);
+      }
+    }
   };
-  CATTN_TRACE(0);
-  for (int t = 0; t < AH && t < n; ++t) dma(t);
+  auto parts_with = [&](int i) {  // parts that own a tile at iteration i
+    int k = 0;
+#pragma unroll
+    for (int p = 0; p < SPLIT; ++p) k += (i < L && p * L + i < n) ? 1 : 0;
+    return k;
+  };
+  // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
+  auto later = [&](int i) {
+    int k = 0;
+    for (int x = i + 2; x <= i + AH - 1; ++x) k += parts_with(x);
+    return k * PER_TILE;
+  };
+
+  unroll<AH>([&](auto I) { dma(decltype(I)::value, I); });
   MB::frag qf[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
   wait_vm(0);
   __syncthreads();
-  CATTN_TRACE(1);
 
   float m = kMasked, lsum = 0.f;
   f32x16 oacc[DT];
@@ -188,87 +301,124 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
     for (int dt = 0; dt < DT; ++dt) vf[ks][dt] = MB::frag{};
   {
     MB::frag k0f[KS_D];
-    read_rows<D>(buf(0), r, h, k0f);
+    read_rows<D>(ring, r, h, k0f);
 #pragma unroll
     for (int ks = 0; ks < KS_D; ++ks) sa = MB::run(k0f[ks], qf[ks], sa);
   }
 
-  for (int j = 0; j < n; ++j) {
-    if (j > 0) {
-      tile_barrier(later_tiles(j, n, AH) * PER_TILE);  // tile j+1 landed; tile j-1 is free
-    }
-    CATTN_TRACE(2 + j);
-    if (j + AH < n) dma(j + AH);
-    if (j >= nsb) continue;  // wave-uniform: this wave is done, it only keeps the barriers
-    const int k0 = j * 32;
-    // causal diagonal / ragged end: only the wave's last sub-block
-    if (j == nsb - 1 && ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S)) {
+  auto softmax = [&](const f32x16& s, float mc, f32x16& pv) {
 #pragma unroll
-      for (int a = 0; a < 16; ++a) {
-        const int key = k0 + acc_row(a, h);
-        if (key >= S || (CAUSAL && key > my_q)) sa[a] = kMasked;
+    for (int a = 0; a < 16; ++a) pv[a] = exp2_hw(fmaf(s[a], c, -mc));
+    float ps[8];  // pairwise sum: a short dependency chain
+#pragma unroll
+    for (int a = 0; a < 8; ++a) ps[a] = pv[2 * a] + pv[2 * a + 1];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) ps[a] = ps[2 * a] + ps[2 * a + 1];
+    return (ps[0] + ps[1]) + (ps[2] + ps[3]);
+  };
+
+  for (int i0 = 0; i0 < L; i0 += NB) {
+    unroll<NB>([&](auto slc) {
+      constexpr int sl = decltype(slc)::value;
+      const int i = i0 + sl;
+      if (i >= L) return;
+      if (i > 0) tile_barrier(later(i));  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
+      if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
+      const int j = tb + i;  // key tile of this iteration
+      const int k0 = j * 32;
+      // causal diagonal / ragged end: only the last tile of the wave's queries
+      if (j == nsb - 1 && ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S)) {
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          const int key = k0 + acc_row(a, h);
+          if (key >= S || (CAUSAL && key > my_q)) sa[a] = kMasked;
+        }
       }
-    }
-    MB::frag kf[KS_D];  // K of sub-block j+1 (clamped to the last one)
-    read_rows<D>(buf(j + 1 < nsb ? j + 1 : j), r, h, kf);
-    __builtin_amdgcn_sched_barrier(0);  // issue the K reads before anything below
-    // Softmax of S(j).  The offset moves (per lane, without a branch) only when
-    // the block max exceeds it by more than 2^kRescaleLog2 in probability
-    // units; alpha rescales the running sum here and O below.
-    float mx = sa[0];
+      // K of the next tile.  On a wave's last iteration this slot holds another
+      // tile (or nothing yet); the product is computed and discarded.
+      MB::frag kf[KS_D];
+      read_rows<D>(ring + ((sl + 1) % NB) * SET, r, h, kf);
+      __builtin_amdgcn_sched_barrier(0);  // issue the K reads before anything below
+      f32x16 pv;
+      float psum = softmax(sa, m * c, pv);
+      // matrix cores, independent of the softmax: O += P(j-1) V(j-1), S(j+1) = K Q^T
 #pragma unroll
-    for (int a = 1; a < 16; ++a) mx = fmaxf(mx, sa[a]);
-    mx = halves_max(mx);
-    const float m_use = (j == 0 || (mx - m) * c > kRescaleLog2) ? mx : m;
-    const float alpha = exp2_hw((m - m_use) * c);  // 0 on the first block, 1 when unchanged
-    m = m_use;
-    const float mc = m * c;
-    float pv[16];
-    float psum = 0.f;
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-    for (int a = 0; a < 16; ++a) {
-      pv[a] = exp2_hw(fmaf(sa[a], c, -mc));
-      psum += pv[a];
-    }
-    lsum = fmaf(lsum, alpha, psum);
-    // matrix cores, independent of the softmax: O += P(j-1) V(j-1), S(j+1) = K Q^T
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pp[ks], oacc[dt]);
+      f32x16 sn = f32x16{};
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+      for (int ks = 0; ks < KS_D; ++ks) sn = MB::run(kf[ks], qf[ks], sn);
+      MB::frag pn[2];
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pp[ks], oacc[dt]);
-    f32x16 sn = f32x16{};
+      for (int ks = 0; ks < 2; ++ks) pn[ks] = MB::pack(pv, ks);
 #pragma unroll
-    for (int ks = 0; ks < KS_D; ++ks) sn = MB::run(kf[ks], qf[ks], sn);
+      for (int e = 0; e < 2 * DT + KS_D; ++e) {  // interleave matrix-core and vector work
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      }
+      // The new P and its sum are finished here, above the branch, so that
+      // the exponentials stay in the same block as the contractions.
+      asm volatile("" ::"v"(psum), "v"(pn[0]), "v"(pn[1]));
+      read_trans<D>(ring + sl * SET + TILE, lane, vf);  // V(j), for the next iteration
+      if (__builtin_amdgcn_ballot_w64(!(psum <= kSumMax))) {  // rare: move the offset
+        // keeps this block a real branch: executed speculatively it would make
+        // every iteration wait for the matrix-core accumulation above
+        asm volatile("" ::: "memory");
+        float mx = sa[0];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+        for (int a = 1; a < 16; ++a) mx = fmaxf(mx, sa[a]);
+        const float mnew = fmaxf(m, halves_max(mx));  // same in both halves of a query
+        const float alpha = exp2_hw((m - mnew) * c);  // 0 on the first block
+        m = mnew;
+        psum = softmax(sa, m * c, pv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pp[ks][i] = (bf16)pv[8 * ks + i];
+        for (int ks = 0; ks < 2; ++ks) pn[ks] = MB::pack(pv, ks);
+        lsum *= alpha;
 #pragma unroll
-    for (int i = 0; i < 2 * DT + KS_D; ++i) {  // interleave matrix-core and vector work
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-    }
-    // The new P and the running sum are finished here, above the branch, so
-    // that the exponentials stay in the same block as the contractions.
-    asm volatile("" ::"v"(lsum), "v"(pp[0]), "v"(pp[1]));
-    read_trans<D>(buf(j) + TILE, lane, vf);  // V(j), for the next iteration
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {  // rare: rescale O (after P(j-1) V(j-1))
-      // keeps this block a real branch: executed speculatively it would make
-      // every iteration wait for the matrix-core accumulation above
-      asm volatile("" ::: "memory");
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-    }
-    sa = sn;
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;  // after O += P(j-1) V(j-1)
+      }
+      lsum += psum;
+      pp[0] = pn[0];
+      pp[1] = pn[1];
+      sa = sn;
+    });
   }
-  if (nsb > 0) {  // drain: O += P(last) V(last)
+  if (cnt > 0) {  // drain: O += P(last) V(last)
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pp[ks], oacc[dt]);
   }
 
-  CATTN_TRACE(60);
+  if constexpr (SPLIT == 2) {
+    // Merge the two key parts of each query group: part 1 hands (O, m, l) to
+    // part 0 through LDS, lane to lane (both waves share the same lane layout).
+    wait_vm(0);
+    __syncthreads();  // every wave is done with the rings
+    float* xb = (float*)smem + (size_t)qg * 64 * (2 * DT * 16 + 2);
+    if (part == 1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) xb[(dt * 16 + a) * 64 + lane] = oacc[dt][a];
+      xb[(DT * 16) * 64 + lane] = m;
+      xb[(DT * 16 + 1) * 64 + lane] = lsum;
+    }
+    __syncthreads();
+    if (part == 1) return;
+    const float m1 = xb[(DT * 16) * 64 + lane], l1 = xb[(DT * 16 + 1) * 64 + lane];
+    const float mn = fmaxf(m, m1);
+    const float s0 = exp2_hw((m - mn) * c), s1 = exp2_hw((m1 - mn) * c);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int a = 0; a < 16; ++a) oacc[dt][a] = oacc[dt][a] * s0 + xb[(dt * 16 + a) * 64 + lane] * s1;
+    lsum = lsum * s0 + l1 * s1;
+    m = mn;
+  }
+
   const float l = halves_sum(lsum);
   if (my_q < S) {
     const float inv = 1.0f / l;
@@ -281,26 +431,28 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
                      oacc[dt][4 * g + 2] * inv, oacc[dt][4 * g + 3] * inv);
     if (h == 0) LSE[(int64_t)bh * S + my_q] = (m * c + log2f(l)) * kLn2;
   }
-  CATTN_TRACE(61);
 }
 
 // ---------------------------------------------------------------------------
 // Backward, kernel 1: dQ (reduces over keys).  Also writes, per (batch, head),
 // D = rowsum(dO * O) and LSE * log2(e) into the workspace (rows padded to a
 // multiple of 32 with zeros) for the dK/dV kernel to copy by DMA.
+//
+// dS = P (dP - D) takes one multiply per element: the dP contraction starts
+// from an accumulator holding D and multiplies by -dO, so it yields D - dP.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, int NB>
 __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                                const bf16* __restrict__ V, const bf16* __restrict__ O,
                                                                const bf16* __restrict__ dO,
                                                                const float* __restrict__ LSE, bf16* __restrict__ dQ,
                                                                float* __restrict__ ws, int S, int BH, int n_qtiles,
                                                                float c, float scale) {
-  typedef Ring<D> RG;
-  constexpr int BQ = 128, NB = RG::NBUF, AH = RG::AHEAD, TILE = RG::TILE;
+  typedef TileGeom<D> G;
+  constexpr int BQ = 128, AH = NB - 1, TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
-  constexpr int PER_TILE = 2 * RG::DMA_PER_TENSOR;
-  __shared__ __attribute__((aligned(16))) char smem[NB * 2 * TILE];  // [buffer][K, V]
+  constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR;
+  __shared__ __attribute__((aligned(16))) char smem[NB * 2 * TILE];  // [slot][K, V]
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
@@ -317,12 +469,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int kend_w = qw >= S ? 0 : (CAUSAL ? min(S, qw + 32) : S);
   const int nsb = (kend_w + 31) / 32;
 
-  auto buf = [&](int t) { return smem + (t % NB) * 2 * TILE; };
-  auto dma = [&](int t) {
-    dma_tile<D>(Kb, t * 32, S, buf(t), tid);
-    dma_tile<D>(Vb, t * 32, S, buf(t) + TILE, tid);
+  TileCopy<D> tc;
+  tc.init(w, lane);
+  auto dma = [&](int t, auto slc) {
+    char* dst = smem + decltype(slc)::value * 2 * TILE;
+    tc.copy(Kb, t * 32, S, dst);
+    tc.copy(Vb, t * 32, S, dst + TILE);
   };
-  for (int t = 0; t < AH && t < n; ++t) dma(t);
+  unroll<AH>([&](auto I) {
+    if (decltype(I)::value < n) dma(decltype(I)::value, I);
+  });
   MB::frag qf[KS_D], dof[KS_D], of[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
   load_row_frags<bf16, D>(dO + base, my_q, S, h, dof);
@@ -339,60 +495,70 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
     for (int i = 0; i < 8; ++i) dpart = fmaf((float)dof[ks][i], (float)of[ks][i], dpart);
   const float Dq = halves_sum(dpart);
   const float lse2 = lse * kLog2e;
-  if (h == 0 && my_q < Sp) {
-    ws[(int64_t)bh * Sp + my_q] = my_q < S ? Dq : 0.f;
-    ws[((int64_t)BH + bh) * Sp + my_q] = lse2;
+  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then LSE * log2(e) row
+    float* wsh = ws + (int64_t)bh * 2 * Sp;
+    wsh[my_q] = my_q < S ? Dq : 0.f;
+    wsh[Sp + my_q] = lse2;
   }
+#pragma unroll
+  for (int ks = 0; ks < KS_D; ++ks) dof[ks] = negated(dof[ks]);
+  f32x16 dinit;
+#pragma unroll
+  for (int a = 0; a < 16; ++a) dinit[a] = Dq;
 
   f32x16 dqacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
   MB::frag kf[KS_D], vfr[KS_D];  // row fragments of the current sub-block
-  read_rows<D>(buf(0), r, h, kf);
-  read_rows<D>(buf(0) + TILE, r, h, vfr);
+  read_rows<D>(smem, r, h, kf);
+  read_rows<D>(smem + TILE, r, h, vfr);
 
-  for (int j = 0; j < n; ++j) {
-    if (j > 0) {
-      tile_barrier(later_tiles(j, n, AH) * PER_TILE);
-    }
-    if (j + AH < n) dma(j + AH);
-    if (j >= nsb) continue;
-    MB::frag ktr[2][DT];
-    read_trans<D>(buf(j), lane, ktr);
-    MB::frag kn[KS_D], vn[KS_D];
-    const int jn = j + 1 < nsb ? j + 1 : j;
-    read_rows<D>(buf(jn), r, h, kn);
-    read_rows<D>(buf(jn) + TILE, r, h, vn);
-    f32x16 s = f32x16{}, dp = f32x16{};
+  for (int j0 = 0; j0 < n; j0 += NB) {
+    unroll<NB>([&](auto slc) {
+      constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
+      const int j = j0 + sl;
+      if (j >= n) return;
+      if (j > 0) tile_barrier(later_tiles(j, n, AH) * PER_TILE);
+      if (j + AH < n) dma(j + AH, IC<(sl + AH) % NB>{});
+      if (j >= nsb) return;
+      const char* cur = smem + sl * 2 * TILE;
+      const char* nxt = smem + sn * 2 * TILE;  // on a wave's last tile: discarded
+      MB::frag ktr[2][DT];
+      read_trans<D>(cur, lane, ktr);
+      MB::frag kn[KS_D], vn[KS_D];
+      read_rows<D>(nxt, r, h, kn);
+      read_rows<D>(nxt + TILE, r, h, vn);
+      f32x16 s = f32x16{}, dx = dinit;
 #pragma unroll
-    for (int ks = 0; ks < KS_D; ++ks) {
-      s = MB::run(kf[ks], qf[ks], s);
-      dp = MB::run(vfr[ks], dof[ks], dp);
-    }
-    const int k0 = j * 32;
-    if (j == nsb - 1 && ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S)) {
+      for (int ks = 0; ks < KS_D; ++ks) {
+        s = MB::run(kf[ks], qf[ks], s);
+        dx = MB::run(vfr[ks], dof[ks], dx);  // D - dP^T
+      }
+      const int k0 = j * 32;
+      if (j == nsb - 1 && ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S)) {
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          const int key = k0 + acc_row(a, h);
+          if (key >= S || (CAUSAL && key > my_q)) s[a] = kMasked;
+        }
+      }
 #pragma unroll
       for (int a = 0; a < 16; ++a) {
-        const int key = k0 + acc_row(a, h);
-        if (key >= S || (CAUSAL && key > my_q)) s[a] = kMasked;
+        const float p = exp2_hw(fmaf(s[a], c, -lse2));
+        dx[a] = -p * dx[a];  // dS^T = P (dP - D)
       }
-    }
 #pragma unroll
-    for (int a = 0; a < 16; ++a) {
-      const float p = exp2_hw(fmaf(s[a], c, -lse2));
-      dp[a] = p * (dp[a] - Dq);  // dS^T
-    }
+      for (int ks = 0; ks < 2; ++ks) {
+        const MB::frag db = MB::pack(dx, ks);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const MB::frag db = MB::pack(dp, ks);
+        for (int dt = 0; dt < DT; ++dt) dqacc[dt] = MB::run(ktr[ks][dt], db, dqacc[dt]);
+      }
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) dqacc[dt] = MB::run(ktr[ks][dt], db, dqacc[dt]);
-    }
-#pragma unroll
-    for (int ks = 0; ks < KS_D; ++ks) {
-      kf[ks] = kn[ks];
-      vfr[ks] = vn[ks];
-    }
+      for (int ks = 0; ks < KS_D; ++ks) {
+        kf[ks] = kn[ks];
+        vfr[ks] = vn[ks];
+      }
+    });
   }
 
   if (my_q < S) {
@@ -407,9 +573,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 }
 
 // ---------------------------------------------------------------------------
-// Backward, kernel 2: dK, dV (reduces over queries)
+// Backward, kernel 2: dK, dV (reduces over queries).  As in the dQ kernel the
+// dP contraction yields D - dP directly: it starts from the tile's D values
+// and multiplies by -V.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, int NB>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
                                                                  const bf16* __restrict__ K,
                                                                  const bf16* __restrict__ V,
@@ -417,8 +585,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
                                                                  const float* __restrict__ ws,
                                                                  bf16* __restrict__ dK, bf16* __restrict__ dV, int S,
                                                                  int BH, int n_ktiles, float c, float scale) {
-  typedef Ring<D> RG;
-  constexpr int BKV = 128, NB = RG::NBUF, AH = RG::AHEAD, TILE = RG::TILE;
+  typedef TileGeom<D> G;
+  constexpr int BKV = 128, AH = NB - 1, TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats LSE*log2e, 32 floats D
   __shared__ __attribute__((aligned(16))) char smem[NB * BUF];
@@ -431,10 +599,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const bf16* Qb = Q + base;
   const bf16* dOb = dO + base;
   const int Sp = ws_rows(S);
-  const float* Db = ws + (int64_t)bh * Sp;
-  const float* Lb = ws + ((int64_t)BH + bh) * Sp;
+  const float* wsh = ws + (int64_t)bh * 2 * Sp;  // D row, then LSE * log2(e) row
+  // lanes 0..7 copy 8 chunks of LSE*log2e, lanes 8..15 8 chunks of D (rows < Sp: in bounds)
+  const unsigned ld_voff = (unsigned)((lane < 8 ? Sp * 4 : 0) + 16 * (lane & 7));
   // copies per tile issued by this wave: Q and dO, plus the LSE/D copy on wave 0
-  const int per_tile = 2 * RG::DMA_PER_TENSOR + (w == 0 ? 1 : 0);
+  const int per_tile = 2 * G::DMA_PER_TENSOR + (w == 0 ? 1 : 0);
 
   const int k0 = kt * BKV, kw = k0 + 32 * w, my_k = kw + r;
   // 32-query tiles of the workgroup: from the one holding k0 (causal: the loop's
@@ -444,21 +613,25 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const int jb = CAUSAL ? kw / 32 : 0;          // this wave's first sub-block
   const int je = kw >= S ? jb : (S + 31) / 32;  // ... and one past its last
 
-  auto buf = [&](int t) { return smem + (t % NB) * BUF; };
-  auto dma = [&](int t) {
+  TileCopy<D> tc;
+  tc.init(w, lane);
+  auto dma = [&](int t, auto slc) {
     const int row0 = (jt0 + t) * 32;
-    char* b = buf(t);
-    dma_tile<D>(Qb, row0, S, b, tid);
-    dma_tile<D>(dOb, row0, S, b + TILE, tid);
-    if (w == 0 && lane < 16)  // 8 chunks of LSE*log2e, then 8 of D (rows < Sp: in bounds)
-      dma16((lane < 8 ? Lb : Db) + row0 + 4 * (lane & 7), b + 2 * TILE);
+    char* b = smem + decltype(slc)::value * BUF;
+    tc.copy(Qb, row0, S, b);
+    tc.copy(dOb, row0, S, b + TILE);
+    if (w == 0 && lane < 16) dma16(wsh + row0, ld_voff, lds_addr(b + 2 * TILE));
   };
-  for (int t = 0; t < AH && t < n; ++t) dma(t);
+  unroll<AH>([&](auto I) {
+    if (decltype(I)::value < n) dma(decltype(I)::value, I);
+  });
   MB::frag kf[KS_D], vf[KS_D];
   load_row_frags<bf16, D>(K + base, my_k, S, h, kf);
   load_row_frags<bf16, D>(V + base, my_k, S, h, vf);
   wait_vm(0);
   __syncthreads();
+#pragma unroll
+  for (int ks = 0; ks < KS_D; ++ks) vf[ks] = negated(vf[ks]);
 
   f32x16 dkacc[DT], dvacc[DT];
 #pragma unroll
@@ -468,70 +641,77 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   }
   MB::frag qf[KS_D], dof[KS_D];  // row fragments of the current sub-block
 
-  for (int t = 0; t < n; ++t) {
-    if (t > 0) {
-      tile_barrier(later_tiles(t, n, AH) * per_tile);
-    }
-    if (t + AH < n) dma(t + AH);
-    const int j = jt0 + t;            // global sub-block index
-    if (j < jb || j >= je) continue;  // wave-uniform
-    const char* lq = buf(t);
-    const char* ldo = lq + TILE;
-    const float* llse = (const float*)(lq + 2 * TILE);
-    const float* ld = llse + 32;
-    if (j == jb) {  // a wave's first sub-block can be any tile: read it here
-      read_rows<D>(lq, r, h, qf);
-      read_rows<D>(ldo, r, h, dof);
-    }
-    MB::frag dotr[2][DT], qtr[2][DT];
-    read_trans<D>(ldo, lane, dotr);
-    read_trans<D>(lq, lane, qtr);
-    MB::frag qn[KS_D], don[KS_D];
-    const int tn = j + 1 < je ? t + 1 : t;
-    read_rows<D>(buf(tn), r, h, qn);
-    read_rows<D>(buf(tn) + TILE, r, h, don);
-    f32x16 s = f32x16{}, dp = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < KS_D; ++ks) {
-      s = MB::run(qf[ks], kf[ks], s);
-      dp = MB::run(dof[ks], vf[ks], dp);
-    }
-    // s[a], dp[a]: query 32j + acc_row(a, h), key my_k
-    const int qs = j * 32;
-    if ((CAUSAL && j == jb) || qs + 32 > S) {
-#pragma unroll
-      for (int a = 0; a < 16; ++a) {
-        const int qry = qs + acc_row(a, h);
-        if (qry >= S || (CAUSAL && my_k > qry)) s[a] = kMasked;
+  for (int t0 = 0; t0 < n; t0 += NB) {
+    unroll<NB>([&](auto slc) {
+      constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
+      const int t = t0 + sl;
+      if (t >= n) return;
+      if (t > 0) tile_barrier(later_tiles(t, n, AH) * per_tile);
+      if (t + AH < n) dma(t + AH, IC<(sl + AH) % NB>{});
+      const int j = jt0 + t;  // global sub-block index
+      if (j < jb || j >= je) return;  // wave-uniform
+      const char* lq = smem + sl * BUF;
+      const char* ldo = lq + TILE;
+      const float* llse = (const float*)(lq + 2 * TILE);
+      const float* ld = llse + 32;
+      if (j == jb) {  // a wave's first sub-block can be any tile: read it here
+        read_rows<D>(lq, r, h, qf);
+        read_rows<D>(ldo, r, h, dof);
       }
-    }
+      MB::frag dotr[2][DT], qtr[2][DT];
+      read_trans<D>(ldo, lane, dotr);
+      read_trans<D>(lq, lane, qtr);
+      MB::frag qn[KS_D], don[KS_D];  // on a wave's last tile: discarded
+      read_rows<D>(smem + sn * BUF, r, h, qn);
+      read_rows<D>(smem + sn * BUF + TILE, r, h, don);
+      f32x16 s = f32x16{}, dx;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *(const f32x4*)(llse + 8 * g + 4 * h);
-      const f32x4 d4 = *(const f32x4*)(ld + 8 * g + 4 * h);
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 d4 = *(const f32x4*)(ld + 8 * g + 4 * h);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int a = 4 * g + i;
-        const float p = exp2_hw(fmaf(s[a], c, -l4[i]));
-        s[a] = p;
-        dp[a] = p * (dp[a] - d4[i]);  // dS
+        for (int i = 0; i < 4; ++i) dx[4 * g + i] = d4[i];
       }
-    }
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const MB::frag pb = MB::pack(s, ks);
-      const MB::frag db = MB::pack(dp, ks);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        dvacc[dt] = MB::run(dotr[ks][dt], pb, dvacc[dt]);
-        dkacc[dt] = MB::run(qtr[ks][dt], db, dkacc[dt]);
+      for (int ks = 0; ks < KS_D; ++ks) {
+        s = MB::run(qf[ks], kf[ks], s);
+        dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
       }
-    }
+      // s[a], dx[a]: query 32j + acc_row(a, h), key my_k
+      const int qs = j * 32;
+      if ((CAUSAL && j == jb) || qs + 32 > S) {
 #pragma unroll
-    for (int ks = 0; ks < KS_D; ++ks) {
-      qf[ks] = qn[ks];
-      dof[ks] = don[ks];
-    }
+        for (int a = 0; a < 16; ++a) {
+          const int qry = qs + acc_row(a, h);
+          if (qry >= S || (CAUSAL && my_k > qry)) s[a] = kMasked;
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 l4 = *(const f32x4*)(llse + 8 * g + 4 * h);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int a = 4 * g + i;
+          const float p = exp2_hw(fmaf(s[a], c, -l4[i]));
+          s[a] = p;
+          dx[a] = -p * dx[a];  // dS = P (dP - D)
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const MB::frag pb = MB::pack(s, ks);
+        const MB::frag db = MB::pack(dx, ks);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          dvacc[dt] = MB::run(dotr[ks][dt], pb, dvacc[dt]);
+          dkacc[dt] = MB::run(qtr[ks][dt], db, dkacc[dt]);
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS_D; ++ks) {
+        qf[ks] = qn[ks];
+        dof[ks] = don[ks];
+      }
+    });
   }
 
   if (my_k < S) {
@@ -552,12 +732,23 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
+// Forward key-range split and ring depth: two parts at D = 64 (the two rings
+// fit the LDS budget of three workgroups per CU), one part at D = 128.
+template <int D> struct FwdCfg {
+  static constexpr int SPLIT = D == 64 ? 2 : 1;
+  static constexpr int NB = D == 64 ? CATTN_FWD_NB64 : CATTN_FWD_NB128;
+};
+template <int D> struct BwdCfg {
+  static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_BWD_NB128;
+};
+
 template <int D, bool CAUSAL>
 static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
-  const int n_qtiles = (a.S + 127) / 128;
-  hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256), 0,
-                     st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S, a.BH,
-                     n_qtiles, a.scale * kLog2e);
+  constexpr int SPLIT = FwdCfg<D>::SPLIT, NB = FwdCfg<D>::NB, BQ = 128 / SPLIT;
+  const int n_qtiles = (a.S + BQ - 1) / BQ;
+  hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
+                     dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S,
+                     a.BH, n_qtiles, a.scale * kLog2e);
   return hipGetLastError();
 }
 
@@ -568,18 +759,19 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t st) {
 
 template <int D, bool CAUSAL>
 static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
+  constexpr int NB = BwdCfg<D>::NB;
   const float c = a.scale * kLog2e;
   if (phase != 2) {
     const int n_qtiles = (a.S + 127) / 128;
-    hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256),
-                       0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
+    hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
+                       dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
                        (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || phase == 1) return e;
   }
   const int n_ktiles = (a.S + 127) / 128;
-  hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_ktiles)), dim3(256),
-                     0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
+  hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, NB>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
+                     dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
                      (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale);
   return hipGetLastError();
 }

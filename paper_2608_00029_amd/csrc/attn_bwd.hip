@@ -73,9 +73,10 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   float lse2 = 0.f;
   if (my_q < S) lse2 = LSE[(int64_t)bh * S + my_q] * kLog2e;
   const int Sp = ws_rows(S);
-  if (h == 0 && my_q < Sp) {  // workspace: D, then LSE * log2(e); padding rows are zero
-    Dvec[(int64_t)bh * Sp + my_q] = my_q < S ? Dq : 0.f;
-    Dvec[((int64_t)BH + bh) * Sp + my_q] = lse2;
+  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then LSE * log2(e) row; padding rows are zero
+    float* wsh = Dvec + (int64_t)bh * 2 * Sp;
+    wsh[my_q] = my_q < S ? Dq : 0.f;
+    wsh[Sp + my_q] = lse2;
   }
 
   const int kend = CAUSAL ? min(S, q0 + BQ) : S;
@@ -171,7 +172,7 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
   const T* Qb = Q + base;
   const T* dOb = dO + base;
   const float* Lb = LSE + (int64_t)bh * S;
-  const float* Db = Dvec + (int64_t)bh * ws_rows(S);
+  const float* Db = Dvec + (int64_t)bh * 2 * ws_rows(S);
 
   const int k0 = kt * BKV, kw = k0 + 32 * w, my_k = kw + r;
   typename M::frag kf[KS_D], vf[KS_D];

@@ -159,6 +159,7 @@ hipError_t launch_fwd(const FwdArgs& a, hipStream_t st) {
   return a.D == 64 ? launch_fwd_d<float, 64>(a, st) : launch_fwd_d<float, 128>(a, st);
 }
 
-int64_t fwd_grid_blocks(int BH, int S) { return (int64_t)BH * ((S + 127) / 128); }
+// upper bound over the forward launch shapes (the smallest query tile is 32 rows)
+int64_t fwd_grid_blocks(int BH, int S) { return (int64_t)BH * ((S + 31) / 32); }
 
 }  // namespace cattn
