@@ -17,6 +17,8 @@ baseline.  Prints ONE JSON line.
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import math
 import os
@@ -32,6 +34,39 @@ DEFAULT_WORKLOAD = "gpt2_small_B8_H12_S1024_D64"
 # MI355X dense matrix-core peaks (TFLOP/s): 256 CUs x 2.4 GHz x FLOP/clock/CU
 PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
 HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2608_00029_amd", "csrc")
+
+
+def kernel_source_digest() -> str:
+    """sha256 over the HIP kernel sources (names and bytes), so that a stored
+    counter measurement can be tied to the kernels it was taken on."""
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h"))):
+        h.update(os.path.basename(p).encode())
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE, each scaled by the
+    factor a plain copy of known size gives), or None when there is no such
+    summary or the kernel sources changed since the counters were taken."""
+    path = os.path.join(PROFILES, f"hbm_traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.lstrip().startswith("#"):
+                key, val = line.split(":", 1)
+                fields[key.strip()] = val.strip()
+    if fields.get("kernel_sources_sha256") != kernel_source_digest():
+        return None
+    val = fields.get(f"{kernel}.traffic_bytes_per_launch")
+    return int(float(val)) if val else None
 
 
 def kernel_flops(w):
@@ -89,8 +124,8 @@ def copy_probe(mib: int) -> int:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
@@ -169,7 +204,7 @@ def main() -> int:
     dom = max(per_kernel_ms, key=per_kernel_ms.get)
     achieved = kf[dom] / (per_kernel_ms[dom] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name), "kernel": dom,
                 "flops_per_launch": kf[dom], "mean_launch_us": round(per_kernel_ms[dom] * 1e3, 2)}
 
     line = {

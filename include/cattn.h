@@ -104,7 +104,7 @@ cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v,
  *              bytes, 4-byte aligned.  Its prior contents are ignored.  On
  *              return it holds, as float [B*H][2][Sp] with Sp = S rounded up
  *              to a multiple of 32: row 0 of head bh is D = rowsum(dO * O),
- *              row 1 is LSE * log2(e); entries S..Sp-1 of both rows are 0.
+ *              row 1 is -LSE / scale; entries S..Sp-1 of both rows are 0.
  *   scale, causal: the values the forward was called with.
  */
 cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
@@ -119,10 +119,10 @@ cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
  * cattn_attn_bwd_dq(...) followed by cattn_attn_bwd_dkdv(...) on one stream.
  *
  * cattn_attn_bwd_dq: the kernel that reduces over keys.  Writes dq, and D =
- *   rowsum(dO * O) and LSE * log2(e) into `workspace` in the layout given
+ *   rowsum(dO * O) and -LSE / scale into `workspace` in the layout given
  *   above.  Same argument rules as cattn_attn_bwd for the arguments it takes.
  * cattn_attn_bwd_dkdv: the kernel that reduces over queries.  Reads D and
- *   LSE * log2(e) from `workspace` (bf16: both; float32: D, LSE from `lse`),
+ *   -LSE / scale from `workspace` (bf16: both; float32: D, LSE from `lse`),
  *   which must hold what cattn_attn_bwd_dq wrote for the same
  *   inputs (ordered before this call on `stream`, or otherwise complete).
  *   Writes dk and dv.

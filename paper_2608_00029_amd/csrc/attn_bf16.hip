@@ -187,13 +187,6 @@ __device__ __forceinline__ MB::frag negated(MB::frag f) {
   return __builtin_bit_cast(MB::frag, u);
 }
 
-// Copies issued after tile t+1 and still allowed in flight at the top of
-// tile t, for a ring running AHEAD tiles ahead over n tiles.
-__device__ __forceinline__ int later_tiles(int t, int n, int ahead) {
-  const int k = min(ahead - 2, n - 2 - t);
-  return k > 0 ? k : 0;
-}
-
 // The forward keeps a softmax offset that moves only when a block's partial
 // probability sum exceeds this bound (or is not finite).  Probabilities are
 // then at most 2^32 (offset at most 32 below the running max, base 2), far
@@ -435,7 +428,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
 
 // ---------------------------------------------------------------------------
 // Backward, kernel 1: dQ (reduces over keys).  Also writes, per (batch, head),
-// D = rowsum(dO * O) and LSE * log2(e) into the workspace (rows padded to a
+// D = rowsum(dO * O) and -LSE/scale into the workspace (rows padded to a
 // multiple of 32 with zeros) for the dK/dV kernel to copy by DMA.
 //
 // dS = P (dP - D) takes one multiply per element: the dP contraction starts
@@ -495,10 +488,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
     for (int i = 0; i < 8; ++i) dpart = fmaf((float)dof[ks][i], (float)of[ks][i], dpart);
   const float Dq = halves_sum(dpart);
   const float lse2 = lse * kLog2e;
-  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then LSE * log2(e) row
+  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then -LSE/scale row
     float* wsh = ws + (int64_t)bh * 2 * Sp;
     wsh[my_q] = my_q < S ? Dq : 0.f;
-    wsh[Sp + my_q] = lse2;
+    wsh[Sp + my_q] = my_q < S ? -lse / scale : 0.f;
   }
 #pragma unroll
   for (int ks = 0; ks < KS_D; ++ks) dof[ks] = negated(dof[ks]);
@@ -573,9 +566,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 }
 
 // ---------------------------------------------------------------------------
-// Backward, kernel 2: dK, dV (reduces over queries).  As in the dQ kernel the
-// dP contraction yields D - dP directly: it starts from the tile's D values
-// and multiplies by -V.
+// Backward, kernel 2: dK, dV (reduces over queries).  Both score contractions
+// start from per-query values copied to LDS with the tile: S from -LSE/scale
+// (so P = exp2(scale*log2e * acc)) and dP, multiplied by -V, from D (so the
+// contraction yields D - dP).
 // ---------------------------------------------------------------------------
 template <int D, bool CAUSAL, int NB>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
@@ -588,7 +582,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   typedef TileGeom<D> G;
   constexpr int BKV = 128, AH = NB - 1, TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
-  constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats LSE*log2e, 32 floats D
+  constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats -LSE/scale, 32 floats D
   __shared__ __attribute__((aligned(16))) char smem[NB * BUF];
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
@@ -599,8 +593,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const bf16* Qb = Q + base;
   const bf16* dOb = dO + base;
   const int Sp = ws_rows(S);
-  const float* wsh = ws + (int64_t)bh * 2 * Sp;  // D row, then LSE * log2(e) row
-  // lanes 0..7 copy 8 chunks of LSE*log2e, lanes 8..15 8 chunks of D (rows < Sp: in bounds)
+  const float* wsh = ws + (int64_t)bh * 2 * Sp;  // D row, then -LSE/scale row
+  // lanes 0..7 copy 8 chunks of -LSE/scale, lanes 8..15 8 chunks of D (rows < Sp: in bounds)
   const unsigned ld_voff = (unsigned)((lane < 8 ? Sp * 4 : 0) + 16 * (lane & 7));
   // copies per tile issued by this wave: Q and dO, plus the LSE/D copy on wave 0
   const int per_tile = 2 * G::DMA_PER_TENSOR + (w == 0 ? 1 : 0);
@@ -664,19 +658,23 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       MB::frag qn[KS_D], don[KS_D];  // on a wave's last tile: discarded
       read_rows<D>(smem + sn * BUF, r, h, qn);
       read_rows<D>(smem + sn * BUF + TILE, r, h, don);
-      f32x16 s = f32x16{}, dx;
+      f32x16 s, dx;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const f32x4 l4 = *(const f32x4*)(llse + 8 * g + 4 * h);
         const f32x4 d4 = *(const f32x4*)(ld + 8 * g + 4 * h);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dx[4 * g + i] = d4[i];
+        for (int i = 0; i < 4; ++i) {
+          s[4 * g + i] = l4[i];
+          dx[4 * g + i] = d4[i];
+        }
       }
 #pragma unroll
       for (int ks = 0; ks < KS_D; ++ks) {
         s = MB::run(qf[ks], kf[ks], s);
         dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
       }
-      // s[a], dx[a]: query 32j + acc_row(a, h), key my_k
+      // s[a], dx[a]: S - LSE/scale and D - dP of query 32j + acc_row(a, h), key my_k
       const int qs = j * 32;
       if ((CAUSAL && j == jb) || qs + 32 > S) {
 #pragma unroll
@@ -686,15 +684,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
         }
       }
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 l4 = *(const f32x4*)(llse + 8 * g + 4 * h);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int a = 4 * g + i;
-          const float p = exp2_hw(fmaf(s[a], c, -l4[i]));
-          s[a] = p;
-          dx[a] = -p * dx[a];  // dS = P (dP - D)
-        }
+      for (int a = 0; a < 16; ++a) {
+        const float p = exp2_hw(s[a] * c);
+        s[a] = p;
+        dx[a] = -p * dx[a];  // dS = P (dP - D)
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {

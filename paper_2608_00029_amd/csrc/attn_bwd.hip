@@ -70,13 +70,13 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
     }
   }
   const float Dq = halves_sum(dpart);
-  float lse2 = 0.f;
-  if (my_q < S) lse2 = LSE[(int64_t)bh * S + my_q] * kLog2e;
+  const float lse = my_q < S ? LSE[(int64_t)bh * S + my_q] : 0.f;
+  const float lse2 = lse * kLog2e;
   const int Sp = ws_rows(S);
-  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then LSE * log2(e) row; padding rows are zero
+  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then -LSE/scale row; padding entries are zero
     float* wsh = Dvec + (int64_t)bh * 2 * Sp;
     wsh[my_q] = my_q < S ? Dq : 0.f;
-    wsh[Sp + my_q] = lse2;
+    wsh[Sp + my_q] = my_q < S ? -lse / scale : 0.f;
   }
 
   const int kend = CAUSAL ? min(S, q0 + BQ) : S;

@@ -6,12 +6,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace cattn {
+#include "attn_sched.h"
 
-// Rows per (batch, head) of each backward workspace array: S padded to a
-// multiple of 32 (padding rows hold zeros), so that 32-row tiles of it can be
-// copied whole.
-__host__ __device__ inline int ws_rows(int S) { return (S + 31) / 32 * 32; }
+namespace cattn {
 
 struct FwdArgs {
   const void* q;
@@ -35,7 +32,7 @@ struct BwdArgs {
   void* dq;
   void* dk;
   void* dv;
-  float* ws;  // workspace: D = rowsum(dO * O) then LSE * log2(e), each [BH, ws_rows(S)] float
+  float* ws;  // workspace, per head: D = rowsum(dO * O) row, then -LSE/scale row, ws_rows(S) floats each
   int BH, S, D;
   float scale;
   bool causal;

@@ -189,13 +189,12 @@ def test_bwd_phases_match_fused_call(cuda):
         dk, dv = attn_bwd_dkdv(q, k, v, do, lse, ws, 0.125, True)
         torch.cuda.synchronize()
         assert torch.equal(g[0], dq) and torch.equal(g[1], dk) and torch.equal(g[2], dv)
-        # workspace, per head: D = rowsum(dO * O) row, then LSE * log2(e) row,
+        # workspace, per head: D = rowsum(dO * O) row, then -LSE/scale row,
         # each padded to a multiple of 32 entries with zeros
         B, H, S = q.shape[:3]
         Sp = (S + 31) // 32 * 32
         wsv = ws.double().reshape(B * H, 2, Sp)
         ref_d = (do.double() * o.double()).sum(-1).reshape(B * H, S)
         assert torch.allclose(wsv[:, 0, :S], ref_d, rtol=1e-5, atol=1e-4)
-        assert torch.allclose(wsv[:, 1, :S], lse.double().reshape(B * H, S) * math.log2(math.e),
-                              rtol=1e-6, atol=1e-6)
+        assert torch.allclose(wsv[:, 1, :S], -lse.double().reshape(B * H, S) / 0.125, rtol=1e-6, atol=1e-6)
         assert torch.all(wsv[:, :, S:] == 0)
