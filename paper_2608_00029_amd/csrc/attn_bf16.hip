@@ -48,6 +48,12 @@ template <int N> using IC = std::integral_constant<int, N>;
 #ifndef CATTN_BWD_NB128
 #define CATTN_BWD_NB128 4
 #endif
+#ifndef CATTN_FWD_SPLIT_MODE  // forward key split at D = 64: 0 by grid size, 1 always, 2 never
+#define CATTN_FWD_SPLIT_MODE 0
+#endif
+#ifndef CATTN_DKDV_NB64S  // dK/dV at D = 64 with the query range split in two (two rings)
+#define CATTN_DKDV_NB64S 4
+#endif
 
 // f(IC<0>{}), f(IC<1>{}), ..., f(IC<N-1>{}), in order.
 template <typename F, int... I>
@@ -570,8 +576,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 // start from per-query values copied to LDS with the tile: S from -LSE/scale
 // (so P = exp2(scale*log2e * acc)) and dP, multiplied by -V, from D (so the
 // contraction yields D - dP).
+//
+// A workgroup owns 32*KG keys of one (batch, head), KG = 4/SPLIT key groups of
+// 32 (one per wave), and splits the query tiles it must visit into SPLIT
+// consecutive parts: wave w takes key group w % KG and query part w / KG.
+// Each part streams its own ring of Q/dO tiles, so the sequential chain of a
+// wave is 1/SPLIT of the query range (the heaviest causal key tile sees every
+// query tile).  With SPLIT = 2 the partial dK, dV of the two parts are added
+// lane to lane through LDS at the end (fixed order: deterministic, no atomics).
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
                                                                  const bf16* __restrict__ K,
                                                                  const bf16* __restrict__ V,
@@ -580,13 +594,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
                                                                  bf16* __restrict__ dK, bf16* __restrict__ dV, int S,
                                                                  int BH, int n_ktiles, float c, float scale) {
   typedef TileGeom<D> G;
-  constexpr int BKV = 128, AH = NB - 1, TILE = G::TILE;
+  constexpr int KG = 4 / SPLIT, BKV = 32 * KG;
+  constexpr int AH = NB - 1, TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats -LSE/scale, 32 floats D
-  __shared__ __attribute__((aligned(16))) char smem[NB * BUF];
+  __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * BUF];  // [part][slot]
+  static_assert(SPLIT == 1 || KG * 64 * (4 * DT * 16) * 4 <= SPLIT * NB * BUF, "merge area");
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
+  const int kg = w % KG, part = w / KG;
   int bh, kt;
   tile_of_block(blockIdx.x, BH, n_ktiles, false, bh, kt);
   const int64_t base = (int64_t)bh * S * D;
@@ -596,29 +613,44 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const float* wsh = ws + (int64_t)bh * 2 * Sp;  // D row, then -LSE/scale row
   // lanes 0..7 copy 8 chunks of -LSE/scale, lanes 8..15 8 chunks of D (rows < Sp: in bounds)
   const unsigned ld_voff = (unsigned)((lane < 8 ? Sp * 4 : 0) + 16 * (lane & 7));
-  // copies per tile issued by this wave: Q and dO, plus the LSE/D copy on wave 0
+  // copies per tile of one part issued by this wave: Q and dO, plus the LSE/D copy on wave 0
   const int per_tile = 2 * G::DMA_PER_TENSOR + (w == 0 ? 1 : 0);
 
-  const int k0 = kt * BKV, kw = k0 + 32 * w, my_k = kw + r;
+  const int k0 = kt * BKV, kw = k0 + 32 * kg, my_k = kw + r;
   // 32-query tiles of the workgroup: from the one holding k0 (causal: the loop's
   // lower bound is raised to the diagonal) to the end of the sequence.
   const int jt0 = CAUSAL ? k0 / 32 : 0;
   const int n = (S + 31) / 32 - jt0;
+  const int L = (n + SPLIT - 1) / SPLIT;        // tiles per part (the last may be short)
   const int jb = CAUSAL ? kw / 32 : 0;          // this wave's first sub-block
   const int je = kw >= S ? jb : (S + 31) / 32;  // ... and one past its last
+  const int tb = part * L;                      // this wave's part: tiles [tb, min(n, tb + L))
+  const int jfirst = max(jb, jt0 + tb);         // first sub-block this wave computes
 
   TileCopy<D> tc;
   tc.init(w, lane);
-  auto dma = [&](int t, auto slc) {
-    const int row0 = (jt0 + t) * 32;
-    char* b = smem + decltype(slc)::value * BUF;
-    tc.copy(Qb, row0, S, b);
-    tc.copy(dOb, row0, S, b + TILE);
-    if (w == 0 && lane < 16) dma16(wsh + row0, ld_voff, lds_addr(b + 2 * TILE));
+  auto has = [&](int p, int i) { return i < L && p * L + i < n; };  // part p owns a tile at iteration i
+  auto dma = [&](int i, auto slc) {  // iteration i's tile of every part, into ring slot slc
+#pragma unroll
+    for (int p = 0; p < SPLIT; ++p) {
+      if (has(p, i)) {
+        const int row0 = (jt0 + p * L + i) * 32;
+        char* b = smem + (p * NB + decltype(slc)::value) * BUF;
+        tc.copy(Qb, row0, S, b);
+        tc.copy(dOb, row0, S, b + TILE);
+        if (w == 0 && lane < 16) dma16(wsh + row0, ld_voff, lds_addr(b + 2 * TILE));
+      }
+    }
   };
-  unroll<AH>([&](auto I) {
-    if (decltype(I)::value < n) dma(decltype(I)::value, I);
-  });
+  // this wave's copies issued after iteration i+1's and still allowed in flight at the top of iteration i
+  auto later = [&](int i) {
+    int k = 0;
+    for (int x = i + 2; x <= i + AH - 1; ++x)
+#pragma unroll
+      for (int p = 0; p < SPLIT; ++p) k += has(p, x) ? 1 : 0;
+    return k * per_tile;
+  };
+  unroll<AH>([&](auto I) { dma(decltype(I)::value, I); });
   MB::frag kf[KS_D], vf[KS_D];
   load_row_frags<bf16, D>(K + base, my_k, S, h, kf);
   load_row_frags<bf16, D>(V + base, my_k, S, h, vf);
@@ -634,39 +666,40 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
     dvacc[dt] = f32x16{};
   }
   MB::frag qf[KS_D], dof[KS_D];  // row fragments of the current sub-block
+  const char* ring = smem + part * NB * BUF;
 
-  for (int t0 = 0; t0 < n; t0 += NB) {
+  for (int i0 = 0; i0 < L; i0 += NB) {
     unroll<NB>([&](auto slc) {
       constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
-      const int t = t0 + sl;
-      if (t >= n) return;
-      if (t > 0) tile_barrier(later_tiles(t, n, AH) * per_tile);
-      if (t + AH < n) dma(t + AH, IC<(sl + AH) % NB>{});
-      const int j = jt0 + t;  // global sub-block index
-      if (j < jb || j >= je) return;  // wave-uniform
-      const char* lq = smem + sl * BUF;
+      const int i = i0 + sl;
+      if (i >= L) return;
+      if (i > 0) tile_barrier(later(i));  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
+      const int j = jt0 + tb + i;  // global sub-block index
+      if (!has(part, i) || j < jb || j >= je) return;  // wave-uniform
+      const char* lq = ring + sl * BUF;
       const char* ldo = lq + TILE;
       const float* llse = (const float*)(lq + 2 * TILE);
       const float* ld = llse + 32;
-      if (j == jb) {  // a wave's first sub-block can be any tile: read it here
+      if (j == jfirst) {  // a wave's first sub-block can be any tile: read it here
         read_rows<D>(lq, r, h, qf);
         read_rows<D>(ldo, r, h, dof);
       }
       MB::frag dotr[2][DT], qtr[2][DT];
       read_trans<D>(ldo, lane, dotr);
       read_trans<D>(lq, lane, qtr);
-      MB::frag qn[KS_D], don[KS_D];  // on a wave's last tile: discarded
-      read_rows<D>(smem + sn * BUF, r, h, qn);
-      read_rows<D>(smem + sn * BUF + TILE, r, h, don);
+      MB::frag qn[KS_D], don[KS_D];  // next tile of the part (on a wave's last tile: discarded)
+      read_rows<D>(ring + sn * BUF, r, h, qn);
+      read_rows<D>(ring + sn * BUF + TILE, r, h, don);
       f32x16 s, dx;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 l4 = *(const f32x4*)(llse + 8 * g + 4 * h);
         const f32x4 d4 = *(const f32x4*)(ld + 8 * g + 4 * h);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          s[4 * g + i] = l4[i];
-          dx[4 * g + i] = d4[i];
+        for (int e = 0; e < 4; ++e) {
+          s[4 * g + e] = l4[e];
+          dx[4 * g + e] = d4[e];
         }
       }
 #pragma unroll
@@ -707,6 +740,32 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
     });
   }
 
+  if constexpr (SPLIT == 2) {
+    // Add the two query parts of each key group: part 1 hands (dK, dV) to
+    // part 0 through LDS, lane to lane (both waves share the same lane layout).
+    wait_vm(0);
+    __syncthreads();  // every wave is done with the rings
+    float* xb = (float*)smem + (size_t)kg * 64 * (4 * DT * 16);
+    if (part == 1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          xb[(dt * 16 + a) * 64 + lane] = dkacc[dt][a];
+          xb[((DT + dt) * 16 + a) * 64 + lane] = dvacc[dt][a];
+        }
+    }
+    __syncthreads();
+    if (part == 1) return;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int a = 0; a < 16; ++a) {
+        dkacc[dt][a] += xb[(dt * 16 + a) * 64 + lane];
+        dvacc[dt][a] += xb[((DT + dt) * 16 + a) * 64 + lane];
+      }
+  }
+
   if (my_k < S) {
     bf16* krow = dK + base + (int64_t)my_k * D;
     bf16* vrow = dV + base + (int64_t)my_k * D;
@@ -725,24 +784,59 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
-// Forward key-range split and ring depth: two parts at D = 64 (the two rings
-// fit the LDS budget of three workgroups per CU), one part at D = 128.
+// Compute units of the current device (queried once per device).
+static int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+// Forward ring depths: per key part when the key range is split in two (two
+// rings of 3 fit the LDS budget of three workgroups per CU), and unsplit.
 template <int D> struct FwdCfg {
-  static constexpr int SPLIT = D == 64 ? 2 : 1;
-  static constexpr int NB = D == 64 ? CATTN_FWD_NB64 : CATTN_FWD_NB128;
+  static constexpr int NB_SPLIT = CATTN_FWD_NB64;
+  static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_FWD_NB128;
 };
 template <int D> struct BwdCfg {
   static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_BWD_NB128;
 };
 
-template <int D, bool CAUSAL>
-static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
-  constexpr int SPLIT = FwdCfg<D>::SPLIT, NB = FwdCfg<D>::NB, BQ = 128 / SPLIT;
+template <int D, bool CAUSAL, int SPLIT, int NB>
+static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
+  constexpr int BKV = 128 / SPLIT;
+  const int n_ktiles = (a.S + BKV - 1) / BKV;
+  hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
+                     dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
+                     (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale);
+  return hipGetLastError();
+}
+
+template <int D, bool CAUSAL, int SPLIT, int NB>
+static hipError_t launch_fwd_split(const FwdArgs& a, hipStream_t st) {
+  constexpr int BQ = 128 / SPLIT;
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S,
                      a.BH, n_qtiles, a.scale * kLog2e);
   return hipGetLastError();
+}
+
+template <int D, bool CAUSAL>
+static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
+  if constexpr (D == 64) {
+    // Split each query tile's key range over two parts when the unsplit grid
+    // (128-query tiles) cannot fill the GPU's workgroup slots (three per CU).
+    const bool split = CATTN_FWD_SPLIT_MODE == 1 ||
+                       (CATTN_FWD_SPLIT_MODE == 0 && (int64_t)a.BH * ((a.S + 127) / 128) < 3 * (int64_t)cu_count());
+    if (split) return launch_fwd_split<D, CAUSAL, 2, FwdCfg<D>::NB_SPLIT>(a, st);
+  }
+  return launch_fwd_split<D, CAUSAL, 1, FwdCfg<D>::NB>(a, st);
 }
 
 hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t st) {
@@ -762,11 +856,15 @@ static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || phase == 1) return e;
   }
-  const int n_ktiles = (a.S + 127) / 128;
-  hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, NB>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
-                     dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
-                     (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale);
-  return hipGetLastError();
+  if constexpr (D == 64) {
+    // Split each key tile's query range over two parts when the unsplit grid
+    // cannot fill the GPU's workgroup slots (two per CU): the heaviest causal
+    // key tile's sequential chain then sets the time.  With a full grid the
+    // unsplit kernel has less overhead per unit of work.
+    if ((int64_t)a.BH * ((a.S + 127) / 128) < 2 * (int64_t)cu_count())
+      return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st);
+  }
+  return launch_dkdv<D, CAUSAL, 1, NB>(a, c, st);
 }
 
 hipError_t launch_bwd_bf16(const BwdArgs& a, int phase, hipStream_t st) {

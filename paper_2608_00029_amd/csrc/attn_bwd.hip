@@ -310,6 +310,7 @@ hipError_t launch_bwd(const BwdArgs& a, int phase, hipStream_t st) {
   return a.D == 64 ? launch_bwd_d<float, 64>(a, phase, st) : launch_bwd_d<float, 128>(a, phase, st);
 }
 
-int64_t bwd_grid_blocks(int BH, int S) { return (int64_t)BH * ((S + 127) / 128); }
+// upper bound over the backward launch shapes (the smallest key tile is 64 rows)
+int64_t bwd_grid_blocks(int BH, int S) { return (int64_t)BH * ((S + 63) / 64); }
 
 }  // namespace cattn
