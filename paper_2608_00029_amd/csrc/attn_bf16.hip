@@ -51,7 +51,7 @@ template <int N> using IC = std::integral_constant<int, N>;
 #ifndef CATTN_FWD_SPLIT_MODE  // forward key split at D = 64: 0 by grid size, 1 always, 2 never
 #define CATTN_FWD_SPLIT_MODE 0
 #endif
-#ifndef CATTN_DKDV_NB64S  // dK/dV at D = 64 with the query range split in two (two rings)
+#ifndef CATTN_DKDV_NB64S  // dQ and dK/dV at D = 64 with the loop range split in two (two rings)
 #define CATTN_DKDV_NB64S 4
 #endif
 
@@ -437,10 +437,15 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
 // D = rowsum(dO * O) and -LSE/scale into the workspace (rows padded to a
 // multiple of 32 with zeros) for the dK/dV kernel to copy by DMA.
 //
+// Like the forward, a workgroup owns 32*QG queries (QG = 4/SPLIT query groups
+// of 32, one per wave) and splits the keys it must visit into SPLIT parts,
+// each streaming its own ring of K/V tiles; with SPLIT = 2 the two partial
+// dQ are added through LDS at the end.
+//
 // dS = P (dP - D) takes one multiply per element: the dP contraction starts
 // from an accumulator holding D and multiplies by -dO, so it yields D - dP.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB>
 __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                                const bf16* __restrict__ V, const bf16* __restrict__ O,
                                                                const bf16* __restrict__ dO,
@@ -448,13 +453,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
                                                                float* __restrict__ ws, int S, int BH, int n_qtiles,
                                                                float c, float scale) {
   typedef TileGeom<D> G;
-  constexpr int BQ = 128, AH = NB - 1, TILE = G::TILE;
+  constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
+  constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR;
-  __shared__ __attribute__((aligned(16))) char smem[NB * 2 * TILE];  // [slot][K, V]
+  __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * SET];  // [part][slot][K, V]
+  static_assert(SPLIT == 1 || QG * 64 * (DT * 16) * 4 <= SPLIT * NB * SET, "merge area");
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
+  const int qg = w % QG, part = w / QG;
   int bh, qt;
   tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
   const int64_t base = (int64_t)bh * S * D;
@@ -462,22 +470,38 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const bf16* Vb = V + base;
   const int Sp = ws_rows(S);
 
-  const int q0 = qt * BQ, qw = q0 + 32 * w, my_q = qw + r;
+  const int q0 = qt * BQ, qw = q0 + 32 * qg, my_q = qw + r;
   const int kend = CAUSAL ? min(S, q0 + BQ) : S;
-  const int n = (kend + 31) / 32;
+  const int n = (kend + 31) / 32;          // 32-key tiles of the workgroup
+  const int L = (n + SPLIT - 1) / SPLIT;   // tiles per part (the last may be short)
   const int kend_w = qw >= S ? 0 : (CAUSAL ? min(S, qw + 32) : S);
-  const int nsb = (kend_w + 31) / 32;
+  const int nsb = (kend_w + 31) / 32;      // tiles this wave's queries need
+  const int tb = part * L;                 // this wave's tiles: [tb, te)
+  const int te = min(nsb, min(n, tb + L));
+  const int cnt = te > tb ? te - tb : 0;
 
   TileCopy<D> tc;
   tc.init(w, lane);
-  auto dma = [&](int t, auto slc) {
-    char* dst = smem + decltype(slc)::value * 2 * TILE;
-    tc.copy(Kb, t * 32, S, dst);
-    tc.copy(Vb, t * 32, S, dst + TILE);
+  auto has = [&](int p, int i) { return i < L && p * L + i < n; };  // part p owns a tile at iteration i
+  auto dma = [&](int i, auto slc) {  // iteration i's tile of every part, into ring slot slc
+#pragma unroll
+    for (int p = 0; p < SPLIT; ++p) {
+      if (has(p, i)) {
+        char* dst = smem + (p * NB + decltype(slc)::value) * SET;
+        tc.copy(Kb, (p * L + i) * 32, S, dst);
+        tc.copy(Vb, (p * L + i) * 32, S, dst + TILE);
+      }
+    }
   };
-  unroll<AH>([&](auto I) {
-    if (decltype(I)::value < n) dma(decltype(I)::value, I);
-  });
+  // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
+  auto later = [&](int i) {
+    int k = 0;
+    for (int x = i + 2; x <= i + AH - 1; ++x)
+#pragma unroll
+      for (int p = 0; p < SPLIT; ++p) k += has(p, x) ? 1 : 0;
+    return k * PER_TILE;
+  };
+  unroll<AH>([&](auto I) { dma(decltype(I)::value, I); });
   MB::frag qf[KS_D], dof[KS_D], of[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
   load_row_frags<bf16, D>(dO + base, my_q, S, h, dof);
@@ -494,7 +518,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
     for (int i = 0; i < 8; ++i) dpart = fmaf((float)dof[ks][i], (float)of[ks][i], dpart);
   const float Dq = halves_sum(dpart);
   const float lse2 = lse * kLog2e;
-  if (h == 0 && my_q < Sp) {  // workspace of this head: D row, then -LSE/scale row
+  if (part == 0 && h == 0 && my_q < Sp) {  // workspace of this head: D row, then -LSE/scale row
     float* wsh = ws + (int64_t)bh * 2 * Sp;
     wsh[my_q] = my_q < S ? Dq : 0.f;
     wsh[Sp + my_q] = my_q < S ? -lse / scale : 0.f;
@@ -508,20 +532,22 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   f32x16 dqacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
+  const char* ring = smem + part * NB * SET;  // this wave's part
   MB::frag kf[KS_D], vfr[KS_D];  // row fragments of the current sub-block
-  read_rows<D>(smem, r, h, kf);
-  read_rows<D>(smem + TILE, r, h, vfr);
+  read_rows<D>(ring, r, h, kf);
+  read_rows<D>(ring + TILE, r, h, vfr);
 
-  for (int j0 = 0; j0 < n; j0 += NB) {
+  for (int i0 = 0; i0 < L; i0 += NB) {
     unroll<NB>([&](auto slc) {
       constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
-      const int j = j0 + sl;
-      if (j >= n) return;
-      if (j > 0) tile_barrier(later_tiles(j, n, AH) * PER_TILE);
-      if (j + AH < n) dma(j + AH, IC<(sl + AH) % NB>{});
-      if (j >= nsb) return;
-      const char* cur = smem + sl * 2 * TILE;
-      const char* nxt = smem + sn * 2 * TILE;  // on a wave's last tile: discarded
+      const int i = i0 + sl;
+      if (i >= L) return;
+      if (i > 0) tile_barrier(later(i));  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
+      if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
+      const int j = tb + i;  // key tile of this iteration
+      const char* cur = ring + sl * SET;
+      const char* nxt = ring + sn * SET;  // on a wave's last tile: another tile, discarded
       MB::frag ktr[2][DT];
       read_trans<D>(cur, lane, ktr);
       MB::frag kn[KS_D], vn[KS_D];
@@ -558,6 +584,26 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
         vfr[ks] = vn[ks];
       }
     });
+  }
+
+  if constexpr (SPLIT == 2) {
+    // Add the two key parts of each query group: part 1 hands dQ to part 0
+    // through LDS, lane to lane (both waves share the same lane layout).
+    wait_vm(0);
+    __syncthreads();  // every wave is done with the rings
+    float* xb = (float*)smem + (size_t)qg * 64 * (DT * 16);
+    if (part == 1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) xb[(dt * 16 + a) * 64 + lane] = dqacc[dt][a];
+    }
+    __syncthreads();
+    if (part == 1) return;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int a = 0; a < 16; ++a) dqacc[dt][a] += xb[(dt * 16 + a) * 64 + lane];
   }
 
   if (my_q < S) {
@@ -808,6 +854,16 @@ template <int D> struct BwdCfg {
 };
 
 template <int D, bool CAUSAL, int SPLIT, int NB>
+static hipError_t launch_dq(const BwdArgs& a, float c, hipStream_t st) {
+  constexpr int BQ = 128 / SPLIT;
+  const int n_qtiles = (a.S + BQ - 1) / BQ;
+  hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
+                     dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
+                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale);
+  return hipGetLastError();
+}
+
+template <int D, bool CAUSAL, int SPLIT, int NB>
 static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
   constexpr int BKV = 128 / SPLIT;
   const int n_ktiles = (a.S + BKV - 1) / BKV;
@@ -848,21 +904,24 @@ template <int D, bool CAUSAL>
 static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   constexpr int NB = BwdCfg<D>::NB;
   const float c = a.scale * kLog2e;
+  // Split the key range of a query tile (dQ), or the query range of a key tile
+  // (dK/dV), over two parts when the unsplit grid cannot fill the GPU's
+  // workgroup slots (two per CU): the heaviest causal tile's sequential chain
+  // then sets the time.  With a full grid the unsplit kernels have less
+  // overhead per unit of work.
+  bool split = false;
+  if constexpr (D == 64) split = (int64_t)a.BH * ((a.S + 127) / 128) < 2 * (int64_t)cu_count();
   if (phase != 2) {
-    const int n_qtiles = (a.S + 127) / 128;
-    hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
-                       dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
-                       (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale);
-    hipError_t e = hipGetLastError();
+    hipError_t e;
+    if constexpr (D == 64) {
+      e = split ? launch_dq<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st) : launch_dq<D, CAUSAL, 1, NB>(a, c, st);
+    } else {
+      e = launch_dq<D, CAUSAL, 1, NB>(a, c, st);
+    }
     if (e != hipSuccess || phase == 1) return e;
   }
   if constexpr (D == 64) {
-    // Split each key tile's query range over two parts when the unsplit grid
-    // cannot fill the GPU's workgroup slots (two per CU): the heaviest causal
-    // key tile's sequential chain then sets the time.  With a full grid the
-    // unsplit kernel has less overhead per unit of work.
-    if ((int64_t)a.BH * ((a.S + 127) / 128) < 2 * (int64_t)cu_count())
-      return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st);
+    if (split) return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st);
   }
   return launch_dkdv<D, CAUSAL, 1, NB>(a, c, st);
 }
