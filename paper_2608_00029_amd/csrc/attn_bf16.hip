@@ -51,6 +51,9 @@ template <int N> using IC = std::integral_constant<int, N>;
 #ifndef CATTN_FWD_SPLIT_MODE  // forward key split at D = 64: 0 by grid size, 1 always, 2 never
 #define CATTN_FWD_SPLIT_MODE 0
 #endif
+#ifndef CATTN_BWD_SPLIT_WG_PER_CU  // backward at D = 64: split below this many unsplit workgroups per CU
+#define CATTN_BWD_SPLIT_WG_PER_CU 2
+#endif
 #ifndef CATTN_DKDV_NB64S  // dQ and dK/dV at D = 64 with the loop range split in two (two rings)
 #define CATTN_DKDV_NB64S 4
 #endif
@@ -112,6 +115,13 @@ __device__ __forceinline__ void tile_barrier(int n) {
   asm volatile("s_barrier" ::: "memory");
 }
 
+// tile_barrier(N) for a compile-time N: a single s_waitcnt.
+template <int N> __device__ __forceinline__ void tile_barrier_c() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // Byte address of an LDS location (the value M0 takes).
 __device__ __forceinline__ unsigned lds_addr(const char* p) {
   return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
@@ -151,6 +161,13 @@ template <int D> struct TileCopy {
       const int row = p / G::CPR;
       voff[i] = (unsigned)(row * D * 2 + (((p % G::CPR) ^ swz(row)) << 4));
     }
+  }
+  // a tile known to lie inside the sequence (row0 + 32 <= nrows)
+  __device__ __forceinline__ void copy_full(const bf16* g, int row0, char* lds) const {
+    const bf16* src = g + (int64_t)row0 * D;
+    const unsigned dst = lds_addr(lds) + w * 64 * 16;
+#pragma unroll
+    for (int i = 0; i < G::DMA_PER_TENSOR; ++i) dma16(src, voff[i], dst + i * 256 * 16);
   }
   __device__ __forceinline__ void copy(const bf16* g, int row0, int nrows, char* lds) const {
     const bf16* src = g + (int64_t)row0 * D;
@@ -630,6 +647,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 // wave is 1/SPLIT of the query range (the heaviest causal key tile sees every
 // query tile).  With SPLIT = 2 the partial dK, dV of the two parts are added
 // lane to lane through LDS at the end (fixed order: deterministic, no atomics).
+//
+// Every per-iteration decision is a compare against an index computed once
+// per wave (the first and last active iteration, the one holding the causal
+// diagonal, the ragged tile), and every wave issues the same copies per tile,
+// so that the common wait at the barrier is a compile-time count.
 // ---------------------------------------------------------------------------
 template <int D, bool CAUSAL, int SPLIT, int NB>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
@@ -644,6 +666,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   constexpr int AH = NB - 1, TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats -LSE/scale, 32 floats D
+  // copies per part tile issued by every wave: its share of Q and dO, and 4 of the 16 LSE/D chunks
+  constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR + 1;
   __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * BUF];  // [part][slot]
   static_assert(SPLIT == 1 || KG * 64 * (4 * DT * 16) * 4 <= SPLIT * NB * BUF, "merge area");
 
@@ -657,46 +681,60 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const bf16* dOb = dO + base;
   const int Sp = ws_rows(S);
   const float* wsh = ws + (int64_t)bh * 2 * Sp;  // D row, then -LSE/scale row
-  // lanes 0..7 copy 8 chunks of -LSE/scale, lanes 8..15 8 chunks of D (rows < Sp: in bounds)
-  const unsigned ld_voff = (unsigned)((lane < 8 ? Sp * 4 : 0) + 16 * (lane & 7));
-  // copies per tile of one part issued by this wave: Q and dO, plus the LSE/D copy on wave 0
-  const int per_tile = 2 * G::DMA_PER_TENSOR + (w == 0 ? 1 : 0);
+  // The 16 chunks of 4 floats that follow a Q/dO tile in LDS -- 8 of
+  // -LSE/scale, then 8 of D -- are copied by lanes 0..3 of every wave: chunk
+  // q = 4w + lane (rows < Sp: in bounds).
+  const int ldq = 4 * w + (lane & 3);
+  const unsigned ld_voff = (unsigned)((ldq < 8 ? Sp + 4 * ldq : 4 * (ldq - 8)) * 4);
 
   const int k0 = kt * BKV, kw = k0 + 32 * kg, my_k = kw + r;
   // 32-query tiles of the workgroup: from the one holding k0 (causal: the loop's
   // lower bound is raised to the diagonal) to the end of the sequence.
   const int jt0 = CAUSAL ? k0 / 32 : 0;
   const int n = (S + 31) / 32 - jt0;
-  const int L = (n + SPLIT - 1) / SPLIT;        // tiles per part (the last may be short)
+  const int L = (n + SPLIT - 1) / SPLIT;        // iterations; part p owns tiles [p*L, min(n, p*L + L))
+  const int n_last = n - (SPLIT - 1) * L;       // tiles of the last part (<= L)
   const int jb = CAUSAL ? kw / 32 : 0;          // this wave's first sub-block
   const int je = kw >= S ? jb : (S + 31) / 32;  // ... and one past its last
-  const int tb = part * L;                      // this wave's part: tiles [tb, min(n, tb + L))
-  const int jfirst = max(jb, jt0 + tb);         // first sub-block this wave computes
+  const int tb = part * L;                      // this wave's part starts at tile tb
+  // iteration indices, relative to this wave's part
+  const int i_lo = max(0, jb - jt0 - tb);                                         // first active
+  const int i_span = max(0, min(part == SPLIT - 1 ? n_last : L, je - jt0 - tb) - i_lo);  // active count
+  const int i_diag = CAUSAL ? jb - jt0 - tb : -1;                                 // causal diagonal
+  const int t_rag = (S % 32) ? (S - 1) / 32 - jt0 : -1;                           // ragged tile (workgroup index)
+  const int i_rag = t_rag - tb;                                                   // ... in this part
+  // copies: iteration x of the ring holds tile p*L + x of every part p with x < L (x < n_last for the last)
+  const int x_full = n_last;  // iterations below this have a tile in every part
 
   TileCopy<D> tc;
   tc.init(w, lane);
-  auto has = [&](int p, int i) { return i < L && p * L + i < n; };  // part p owns a tile at iteration i
-  auto dma = [&](int i, auto slc) {  // iteration i's tile of every part, into ring slot slc
+  auto dma = [&](int x, auto slc) {  // iteration x's tile of every part, into ring slot slc
 #pragma unroll
     for (int p = 0; p < SPLIT; ++p) {
-      if (has(p, i)) {
-        const int row0 = (jt0 + p * L + i) * 32;
+      if (p < SPLIT - 1 || x < n_last) {
+        const int t = p * L + x;
+        const int row0 = (jt0 + t) * 32;
         char* b = smem + (p * NB + decltype(slc)::value) * BUF;
-        tc.copy(Qb, row0, S, b);
-        tc.copy(dOb, row0, S, b + TILE);
-        if (w == 0 && lane < 16) dma16(wsh + row0, ld_voff, lds_addr(b + 2 * TILE));
+        if (t != t_rag) {
+          tc.copy_full(Qb, row0, b);
+          tc.copy_full(dOb, row0, b + TILE);
+        } else {
+          tc.copy(Qb, row0, S, b);
+          tc.copy(dOb, row0, S, b + TILE);
+        }
+        if (lane < 4) dma16(wsh + row0, ld_voff, lds_addr(b + 2 * TILE) + 64 * w);
       }
     }
   };
-  // this wave's copies issued after iteration i+1's and still allowed in flight at the top of iteration i
+  // copies of this wave issued after iteration i+1's and still allowed in flight at the top of iteration i
   auto later = [&](int i) {
     int k = 0;
-    for (int x = i + 2; x <= i + AH - 1; ++x)
-#pragma unroll
-      for (int p = 0; p < SPLIT; ++p) k += has(p, x) ? 1 : 0;
-    return k * per_tile;
+    for (int x = i + 2; x <= i + AH - 1; ++x) k += (x < L ? SPLIT - 1 : 0) + (x < n_last ? 1 : 0);
+    return k * PER_TILE;
   };
-  unroll<AH>([&](auto I) { dma(decltype(I)::value, I); });
+  unroll<AH>([&](auto I) {
+    if (decltype(I)::value < L) dma(decltype(I)::value, I);
+  });
   MB::frag kf[KS_D], vf[KS_D];
   load_row_frags<bf16, D>(K + base, my_k, S, h, kf);
   load_row_frags<bf16, D>(V + base, my_k, S, h, vf);
@@ -719,15 +757,20 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) tile_barrier(later(i));  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i > 0) {  // iteration i+1's tiles landed; iteration i-1's slots are free
+        if (i + AH - 1 < x_full) {
+          tile_barrier_c<(AH - 2) * SPLIT * PER_TILE>();
+        } else {
+          tile_barrier(later(i));
+        }
+      }
       if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
-      const int j = jt0 + tb + i;  // global sub-block index
-      if (!has(part, i) || j < jb || j >= je) return;  // wave-uniform
+      if ((unsigned)(i - i_lo) >= (unsigned)i_span) return;  // wave-uniform: not an active sub-block
       const char* lq = ring + sl * BUF;
       const char* ldo = lq + TILE;
       const float* llse = (const float*)(lq + 2 * TILE);
       const float* ld = llse + 32;
-      if (j == jfirst) {  // a wave's first sub-block can be any tile: read it here
+      if (i == i_lo) {  // a wave's first sub-block can be any tile: read it here
         read_rows<D>(lq, r, h, qf);
         read_rows<D>(ldo, r, h, dof);
       }
@@ -754,8 +797,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
         dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
       }
       // s[a], dx[a]: S - LSE/scale and D - dP of query 32j + acc_row(a, h), key my_k
-      const int qs = j * 32;
-      if ((CAUSAL && j == jb) || qs + 32 > S) {
+      if (i == i_diag || i == i_rag) {  // the causal diagonal or the ragged end of the sequence
+        const int qs = (jt0 + tb + i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int qry = qs + acc_row(a, h);
@@ -910,7 +953,7 @@ static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   // then sets the time.  With a full grid the unsplit kernels have less
   // overhead per unit of work.
   bool split = false;
-  if constexpr (D == 64) split = (int64_t)a.BH * ((a.S + 127) / 128) < 2 * (int64_t)cu_count();
+  if constexpr (D == 64) split = (int64_t)a.BH * ((a.S + 127) / 128) < CATTN_BWD_SPLIT_WG_PER_CU * (int64_t)cu_count();
   if (phase != 2) {
     hipError_t e;
     if constexpr (D == 64) {
