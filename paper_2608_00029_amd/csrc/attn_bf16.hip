@@ -268,35 +268,42 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const int te = min(nsb, min(n, tb + L));
   const int cnt = te > tb ? te - tb : 0;
 
+  const int n_last = n - (SPLIT - 1) * L;  // tiles of the last part (<= L)
+  // the key tile that holds the ragged end of the sequence, if this workgroup copies one
+  const int t_rag = (S % 32) && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
+  // the iteration (in this wave's part) whose tile must be masked: the wave's
+  // last tile when it straddles the causal diagonal or the end of the sequence
+  const int i_mask = nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
+
   TileCopy<D> tc;
   tc.init(w, lane);
   const char* ring = smem + part * NB * SET;  // this wave's part
-  auto dma = [&](int i, auto slc) {  // iteration i's tile of every part, into ring slot slc
-    constexpr int sl = decltype(slc)::value;
+  auto dma = [&](int x, auto slc) {  // iteration x's tile of every part, into ring slot slc
 #pragma unroll
     for (int p = 0; p < SPLIT; ++p) {
-      const int t = p * L + i;
-      if (i < L && t < n) {
-        char* dst = smem + (p * NB + sl) * SET;
-        tc.copy(Kb, t * 32, S, dst);
-        tc.copy(Vb, t * 32, S, dst + TILE);
+      if (p < SPLIT - 1 || x < n_last) {
+        const int t = p * L + x;
+        char* dst = smem + (p * NB + decltype(slc)::value) * SET;
+        if (t != t_rag) {
+          tc.copy_full(Kb, t * 32, dst);
+          tc.copy_full(Vb, t * 32, dst + TILE);
+        } else {
+          tc.copy(Kb, t * 32, S, dst);
+          tc.copy(Vb, t * 32, S, dst + TILE);
+        }
       }
     }
-  };
-  auto parts_with = [&](int i) {  // parts that own a tile at iteration i
-    int k = 0;
-#pragma unroll
-    for (int p = 0; p < SPLIT; ++p) k += (i < L && p * L + i < n) ? 1 : 0;
-    return k;
   };
   // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
   auto later = [&](int i) {
     int k = 0;
-    for (int x = i + 2; x <= i + AH - 1; ++x) k += parts_with(x);
+    for (int x = i + 2; x <= i + AH - 1; ++x) k += (x < L ? SPLIT - 1 : 0) + (x < n_last ? 1 : 0);
     return k * PER_TILE;
   };
 
-  unroll<AH>([&](auto I) { dma(decltype(I)::value, I); });
+  unroll<AH>([&](auto I) {
+    if (decltype(I)::value < L) dma(decltype(I)::value, I);
+  });
   MB::frag qf[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
   wait_vm(0);
@@ -338,13 +345,18 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       constexpr int sl = decltype(slc)::value;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) tile_barrier(later(i));  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i > 0) {  // iteration i+1's tiles landed; iteration i-1's slots are free
+        if (i + AH - 1 < n_last) {
+          tile_barrier_c<(AH - 2) * SPLIT * PER_TILE>();
+        } else {
+          tile_barrier(later(i));
+        }
+      }
       if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
-      const int j = tb + i;  // key tile of this iteration
-      const int k0 = j * 32;
       // causal diagonal / ragged end: only the last tile of the wave's queries
-      if (j == nsb - 1 && ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S)) {
+      if (i == i_mask) {
+        const int k0 = (tb + i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int key = k0 + acc_row(a, h);
@@ -497,28 +509,40 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int te = min(nsb, min(n, tb + L));
   const int cnt = te > tb ? te - tb : 0;
 
+  const int n_last = n - (SPLIT - 1) * L;  // tiles of the last part (<= L)
+  // the key tile that holds the ragged end of the sequence, if this workgroup copies one
+  const int t_rag = (S % 32) && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
+  // the iteration (in this wave's part) whose tile must be masked: the wave's
+  // last tile when it straddles the causal diagonal or the end of the sequence
+  const int i_mask = nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
+
   TileCopy<D> tc;
   tc.init(w, lane);
-  auto has = [&](int p, int i) { return i < L && p * L + i < n; };  // part p owns a tile at iteration i
-  auto dma = [&](int i, auto slc) {  // iteration i's tile of every part, into ring slot slc
+  auto dma = [&](int x, auto slc) {  // iteration x's tile of every part, into ring slot slc
 #pragma unroll
     for (int p = 0; p < SPLIT; ++p) {
-      if (has(p, i)) {
+      if (p < SPLIT - 1 || x < n_last) {
+        const int t = p * L + x;
         char* dst = smem + (p * NB + decltype(slc)::value) * SET;
-        tc.copy(Kb, (p * L + i) * 32, S, dst);
-        tc.copy(Vb, (p * L + i) * 32, S, dst + TILE);
+        if (t != t_rag) {
+          tc.copy_full(Kb, t * 32, dst);
+          tc.copy_full(Vb, t * 32, dst + TILE);
+        } else {
+          tc.copy(Kb, t * 32, S, dst);
+          tc.copy(Vb, t * 32, S, dst + TILE);
+        }
       }
     }
   };
   // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
   auto later = [&](int i) {
     int k = 0;
-    for (int x = i + 2; x <= i + AH - 1; ++x)
-#pragma unroll
-      for (int p = 0; p < SPLIT; ++p) k += has(p, x) ? 1 : 0;
+    for (int x = i + 2; x <= i + AH - 1; ++x) k += (x < L ? SPLIT - 1 : 0) + (x < n_last ? 1 : 0);
     return k * PER_TILE;
   };
-  unroll<AH>([&](auto I) { dma(decltype(I)::value, I); });
+  unroll<AH>([&](auto I) {
+    if (decltype(I)::value < L) dma(decltype(I)::value, I);
+  });
   MB::frag qf[KS_D], dof[KS_D], of[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
   load_row_frags<bf16, D>(dO + base, my_q, S, h, dof);
@@ -559,7 +583,13 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
       constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) tile_barrier(later(i));  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i > 0) {  // iteration i+1's tiles landed; iteration i-1's slots are free
+        if (i + AH - 1 < n_last) {
+          tile_barrier_c<(AH - 2) * SPLIT * PER_TILE>();
+        } else {
+          tile_barrier(later(i));
+        }
+      }
       if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
       const int j = tb + i;  // key tile of this iteration
@@ -576,8 +606,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
         s = MB::run(kf[ks], qf[ks], s);
         dx = MB::run(vfr[ks], dof[ks], dx);  // D - dP^T
       }
-      const int k0 = j * 32;
-      if (j == nsb - 1 && ((CAUSAL && k0 + 31 > qw) || k0 + 32 > S)) {
+      if (i == i_mask) {
+        const int k0 = j * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int key = k0 + acc_row(a, h);
