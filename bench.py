@@ -9,9 +9,12 @@ time of exactly --steps steps, bracketed by device synchronisations.
 
 The same timed region also records HIP events around each kernel on the
 stream the kernels run on; the slowest kernel's mean duration gives the
-roofline entry.  On rank 0 the float64 CPU oracle is then timed on a bounded
-sample of the same workload (whole (batch, head) slices) as a reported
-baseline.  Prints ONE JSON line.
+roofline entry.  After the timed region every workload (the tiny float32 one,
+GPT-2 small/medium, XL width, long context) is timed too -- forward, backward
+and whole step -- under "configs" (--configs 0 skips it; profile runs do).  On
+rank 0 the float64 CPU oracle is then timed on a bounded sample of the same
+workload (whole (batch, head) slices) as a reported baseline.  Prints ONE JSON
+line.
 """
 
 from __future__ import annotations
@@ -102,10 +105,63 @@ def cpu_baseline(w, inputs, budget_s: float):
     dt = time.perf_counter() - t0
     fwd_f, bwd_f = w.counted_flops()
     per_head = (fwd_f + bwd_f) / (w.B * w.H)
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu_model)
+    except OSError:
+        pass
     return {"value": round(per_head * done / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model,
             "sample": f"{done} of {w.B * w.H} (batch, head) slices of {w.name}, fwd+bwd in float64, "
                       f"{dt:.1f} s wall"}
+
+
+def time_workload(w, bd, steps: int, warmup: int):
+    """Forward, backward (dQ then dK/dV) and whole-step times of one workload,
+    inputs resident in HBM: mean ms over `steps` launches of each, timed with
+    HIP events on the stream the kernels run on."""
+    import ctypes
+    import torch
+    from paper_2608_00029_amd.workloads import workload_inputs
+    dev = torch.device("cuda:0")
+    q, k, v, do = (t.to(dev) for t in workload_inputs(w))
+    o = torch.empty_like(q)
+    lse = torch.empty((w.B, w.H, w.S), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    ws = torch.empty((bd.workspace_bytes(w.B, w.H, w.S, w.D) // 4,), dtype=torch.float32, device=dev)
+    L = bd.lib()
+    stream = torch.cuda.current_stream(dev)
+    shape = (w.B, w.H, w.S, w.D, float(w.scale), int(w.causal), bd.CATTN_BF16 if w.dtype == "bf16" else bd.CATTN_F32,
+             ctypes.c_void_p(stream.cuda_stream))
+    P = lambda t: t.data_ptr()  # noqa: E731
+
+    def fwd():
+        return L.cattn_attn_fwd(P(q), P(k), P(v), P(o), P(lse), *shape)
+
+    def bwd():
+        return L.cattn_attn_bwd(P(q), P(k), P(v), P(o), P(do), P(lse), P(dq), P(dk), P(dv), P(ws), *shape)
+
+    for _ in range(warmup):
+        if fwd() != 0 or bwd() != 0:
+            raise RuntimeError(f"{w.name}: {bd.last_error_string()}")
+    out = {}
+    for name, fs in (("fwd", (fwd,)), ("bwd", (bwd,)), ("step", (fwd, bwd))):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            for f in fs:
+                f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out[name] = e0.elapsed_time(e1) / steps
+    fwd_f, bwd_f = w.counted_flops()
+    return {"fwd_ms": round(out["fwd"], 5), "bwd_ms": round(out["bwd"], 5), "step_ms": round(out["step"], 5),
+            "fwd_tflops": round(fwd_f / (out["fwd"] * 1e-3) / 1e12, 2),
+            "bwd_tflops": round(bwd_f / (out["bwd"] * 1e-3) / 1e12, 2),
+            "step_tflops": round((fwd_f + bwd_f) / (out["step"] * 1e-3) / 1e12, 2),
+            "pct_peak": round(100.0 * (fwd_f + bwd_f) / (out["step"] * 1e-3) / 1e12 / PEAK_TFLOPS[w.dtype], 2)}
 
 
 def copy_probe(mib: int) -> int:
@@ -129,6 +185,8 @@ def main() -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
+    ap.add_argument("--configs", type=int, default=1,
+                    help="also time every workload (forward, backward, step) after the timed region (0 disables)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark, run 5 plain device-to-device copies of this many MiB "
                          "(reference kernel for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -226,6 +284,9 @@ def main() -> int:
         "kernels_us": {n: round(t * 1e3, 2) for n, t in per_kernel_ms.items()},
         "roofline": roofline,
     }
+    if args.configs:
+        from paper_2608_00029_amd.workloads import WORKLOADS
+        line["configs"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in WORKLOADS}
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, cpu_inputs, args.cpu_seconds)
     print(json.dumps(line), flush=True)
