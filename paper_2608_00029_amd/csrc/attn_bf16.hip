@@ -295,11 +295,8 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
     }
   };
   // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
-  auto later = [&](int i) {
-    int k = 0;
-    for (int x = i + 2; x <= i + AH - 1; ++x) k += (x < L ? SPLIT - 1 : 0) + (x < n_last ? 1 : 0);
-    return k * PER_TILE;
-  };
+  constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
+  auto later = [&](int i) { return ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE; };
 
   unroll<AH>([&](auto I) {
     if (decltype(I)::value < L) dma(decltype(I)::value, I);
@@ -345,9 +342,9 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       constexpr int sl = decltype(slc)::value;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) {  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
         if (i + AH - 1 < n_last) {
-          tile_barrier_c<(AH - 2) * SPLIT * PER_TILE>();
+          tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
         } else {
           tile_barrier(later(i));
         }
@@ -535,11 +532,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
     }
   };
   // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
-  auto later = [&](int i) {
-    int k = 0;
-    for (int x = i + 2; x <= i + AH - 1; ++x) k += (x < L ? SPLIT - 1 : 0) + (x < n_last ? 1 : 0);
-    return k * PER_TILE;
-  };
+  constexpr int NEED = 0;  // iteration i reads the tiles of iterations i .. i+NEED
+  auto later = [&](int i) { return ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE; };
   unroll<AH>([&](auto I) {
     if (decltype(I)::value < L) dma(decltype(I)::value, I);
   });
@@ -574,18 +568,15 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
   const char* ring = smem + part * NB * SET;  // this wave's part
-  MB::frag kf[KS_D], vfr[KS_D];  // row fragments of the current sub-block
-  read_rows<D>(ring, r, h, kf);
-  read_rows<D>(ring + TILE, r, h, vfr);
 
   for (int i0 = 0; i0 < L; i0 += NB) {
     unroll<NB>([&](auto slc) {
-      constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
+      constexpr int sl = decltype(slc)::value;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) {  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
         if (i + AH - 1 < n_last) {
-          tile_barrier_c<(AH - 2) * SPLIT * PER_TILE>();
+          tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
         } else {
           tile_barrier(later(i));
         }
@@ -594,12 +585,13 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
       const int j = tb + i;  // key tile of this iteration
       const char* cur = ring + sl * SET;
-      const char* nxt = ring + sn * SET;  // on a wave's last tile: another tile, discarded
+      // this tile's rows are read here rather than one tile ahead: the 32
+      // registers that saves give three waves per SIMD at D = 64
+      MB::frag kf[KS_D], vfr[KS_D];
+      read_rows<D>(cur, r, h, kf);
+      read_rows<D>(cur + TILE, r, h, vfr);
       MB::frag ktr[2][DT];
       read_trans<D>(cur, lane, ktr);
-      MB::frag kn[KS_D], vn[KS_D];
-      read_rows<D>(nxt, r, h, kn);
-      read_rows<D>(nxt + TILE, r, h, vn);
       f32x16 s = f32x16{}, dx = dinit;
 #pragma unroll
       for (int ks = 0; ks < KS_D; ++ks) {
@@ -624,11 +616,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
         const MB::frag db = MB::pack(dx, ks);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) dqacc[dt] = MB::run(ktr[ks][dt], db, dqacc[dt]);
-      }
-#pragma unroll
-      for (int ks = 0; ks < KS_D; ++ks) {
-        kf[ks] = kn[ks];
-        vfr[ks] = vn[ks];
       }
     });
   }
@@ -757,11 +744,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
     }
   };
   // copies of this wave issued after iteration i+1's and still allowed in flight at the top of iteration i
-  auto later = [&](int i) {
-    int k = 0;
-    for (int x = i + 2; x <= i + AH - 1; ++x) k += (x < L ? SPLIT - 1 : 0) + (x < n_last ? 1 : 0);
-    return k * PER_TILE;
-  };
+  constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
+  auto later = [&](int i) { return ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE; };
   unroll<AH>([&](auto I) {
     if (decltype(I)::value < L) dma(decltype(I)::value, I);
   });
@@ -787,9 +771,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) {  // iteration i+1's tiles landed; iteration i-1's slots are free
+      if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
         if (i + AH - 1 < x_full) {
-          tile_barrier_c<(AH - 2) * SPLIT * PER_TILE>();
+          tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
         } else {
           tile_barrier(later(i));
         }

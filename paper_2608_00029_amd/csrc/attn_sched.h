@@ -13,9 +13,21 @@ constexpr int imax(int a, int b) { return a > b ? a : b; }
 // be copied whole.
 constexpr int ws_rows(int S) { return (S + 31) / 32 * 32; }
 
-// Copies issued after tile t+1 and still allowed in flight at the top of
-// tile t, in tiles, for a ring that runs `ahead` tiles ahead over n tiles
-// (tile t+k is copied at the top of tile t+k-ahead).
-constexpr int later_tiles(int t, int n, int ahead) { return imax(0, imin(ahead - 2, n - 2 - t)); }
+// Ring of LDS buffers streamed over iterations 0 .. L-1 by `split` parts: at
+// iteration x every part owns one tile, except that the last part owns tiles
+// only while x < n_last (n_last <= L).  The tiles of iteration x are copied at
+// the top of iteration x - ahead (iterations 0 .. ahead-1 before the loop),
+// each wave issuing the same number of copies per part tile, and a wave's
+// copies complete in issue order.  Iteration i reads the tiles of iterations
+// i .. i+need.  At the top of iteration i a wave may therefore leave in flight
+// the part tiles of iterations i+need+1 .. i+ahead-1; this is their number.
+constexpr int ring_in_flight(int i, int L, int n_last, int split, int ahead, int need) {
+  int k = 0;
+  for (int x = i + need + 1; x <= i + ahead - 1; ++x) k += (x < L ? split - 1 : 0) + (x < n_last ? 1 : 0);
+  return k;
+}
+// The common case, when every part owns a tile at each of those iterations
+// (i + ahead - 1 < n_last): a compile-time count.
+constexpr int ring_in_flight_full(int split, int ahead, int need) { return (ahead - 1 - need) * split; }
 
 }  // namespace cattn

@@ -1,13 +1,6 @@
-// Exhaustive check of the tile-schedule arithmetic of attn_sched.h against the
-// conditions the streaming loops of the bf16 kernels rely on.
-//
-// A loop over n tiles with a ring of NB buffers copies tile k into buffer
-// k % NB at the top of tile k - AHEAD (AHEAD = NB - 1; tiles 0..AHEAD-1 before
-// the loop), each wave issuing a fixed number of copies per tile, and the
-// copies of one wave complete in issue order.  At the top of tile t (t >= 1)
-// the wave waits until at most later_tiles(t, n, AHEAD) tiles of its copies
-// are in flight, then meets the other waves at a barrier; during tile t it
-// reads tiles t and t+1.
+// Exhaustive check of the ring-schedule arithmetic of attn_sched.h against an
+// explicit simulation of the copies, for every ring depth, split and read
+// depth the kernels use and every tile count up to 300.
 #include <cstdio>
 #include <initializer_list>
 
@@ -19,19 +12,32 @@ int main() {
   long bad = 0, checks = 0;
   for (int NB : {3, 4, 6, 8}) {
     const int AH = NB - 1;
-    for (int n = 1; n <= 300; ++n) {
-      for (int t = 1; t < n; ++t) {
-        ++checks;
-        // copies issued before the wait at the top of tile t: tiles 0 .. min(t + AH - 1, n - 1)
-        const int issued = imin(t + AH, n);
-        const int done = issued - later_tiles(t, n, AH);  // tiles 0 .. done-1 have landed
-        if (done < imin(t + 2, n)) ++bad;                  // tiles t and t+1 are resident
-        if (later_tiles(t, n, AH) < 0) ++bad;
-        // the copy issued at the top of tile t (tile t + AH) goes to the buffer of tile
-        // t - 1, which every wave finished before the barrier; never to tile t or t + 1
-        if (t + AH < n) {
-          const int b = (t + AH) % NB;
-          if (b == t % NB || b == (t + 1) % NB || b != (t - 1) % NB) ++bad;
+    for (int split : {1, 2}) {
+      for (int need : {0, 1}) {
+        if (need >= AH) continue;
+        for (int n = 1; n <= 300; ++n) {
+          const int L = (n + split - 1) / split, n_last = n - (split - 1) * L;
+          auto tiles = [&](int x) { return (x < L ? split - 1 : 0) + (x < n_last ? 1 : 0); };
+          for (int i = 1; i < L; ++i) {
+            ++checks;
+            // copies issued before the wait at the top of iteration i, in iteration order:
+            // iterations 0 .. AH-1 before the loop, iteration i'+AH at the top of iteration i' < i
+            int issued = 0;
+            for (int x = 0; x < L && x <= i - 1 + AH; ++x) issued += tiles(x);
+            const int f = ring_in_flight(i, L, n_last, split, AH, need);
+            int required = 0;  // every part tile this iteration reads
+            for (int x = 0; x <= i + need && x < L; ++x) required += tiles(x);
+            if (f < 0 || issued - f < required) ++bad;
+            if (i + AH - 1 < n_last && f != ring_in_flight_full(split, AH, need)) ++bad;
+            // the copy issued at the top of iteration i (iteration i+AH) reuses the buffer
+            // of iteration i-1, finished before the barrier, never one read at i .. i+need
+            if (i + AH < L) {
+              const int b = (i + AH) % NB;
+              if (b != (i - 1) % NB) ++bad;
+              for (int k = 0; k <= need; ++k)
+                if (b == (i + k) % NB) ++bad;
+            }
+          }
         }
       }
     }
