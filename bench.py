@@ -7,11 +7,12 @@ with every input already resident in HBM.  Throughput is the counted causal
 FLOPs of the step (forward 2*B*H*S^2*D, backward 5*B*H*S^2*D) over the wall
 time of exactly --steps steps, bracketed by device synchronisations.
 
-The same timed region also records HIP events around each kernel on the
-stream the kernels run on; the slowest kernel's mean duration gives the
-roofline entry.  After the timed region every workload (the tiny float32 one,
-GPT-2 small/medium, XL width, long context) is timed too -- forward, backward
-and whole step -- under "configs" (--configs 0 skips it; profile runs do).  On
+The same timed region also records HIP events around each kernel, on the
+stream the kernels run on, on every 8th step (--event-every); the slowest
+kernel's mean duration over those launches gives the roofline entry.  After
+the timed region every workload (the tiny float32 one, GPT-2 small/medium, XL
+width, long context) is timed too -- forward, backward and whole step -- under
+"configs" (--configs 0 skips it; profile runs do).  On
 rank 0 the float64 CPU oracle is then timed on a bounded sample of the same
 workload (whole (batch, head) slices) as a reported baseline.  Prints ONE JSON
 line.
@@ -183,6 +184,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=300)
     ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--event-every", type=int, default=8,
+                    help="bracket each kernel with HIP events on every Nth timed step (1: every step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--configs", type=int, default=1,
@@ -239,19 +242,29 @@ def main() -> int:
                 raise RuntimeError(f"{name}: {bd.status_string(st)}: {bd.last_error_string()}")
     torch.cuda.synchronize()
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)] for _ in range(args.steps)]
+    # Every --event-every-th timed step brackets each kernel with HIP events on the
+    # kernels' stream; the other steps run bare.  An event between two kernels
+    # costs the GPU a few microseconds, so recording them on every step would
+    # inflate the step time the throughput is computed from by about a tenth.
+    every = max(1, args.event_every)
+    sampled = [i for i in range(args.steps) if i % every == 0]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)] for _ in sampled]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        e = ev[i]
-        e[0].record(stream)
-        for j, (_, f) in enumerate(kernels):
-            f()
-            e[j + 1].record(stream)
+        if i % every == 0:
+            e = ev[i // every]
+            e[0].record(stream)
+            for j, (_, f) in enumerate(kernels):
+                f()
+                e[j + 1].record(stream)
+        else:
+            for _, f in kernels:
+                f()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
-    per_kernel_ms = {name: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(args.steps)) / args.steps
+    per_kernel_ms = {name: sum(e[j].elapsed_time(e[j + 1]) for e in ev) / len(ev)
                      for j, (name, _) in enumerate(kernels)}
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     fwd_f, bwd_f = w.counted_flops()
@@ -263,7 +276,8 @@ def main() -> int:
     achieved = kf[dom] / (per_kernel_ms[dom] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name), "kernel": dom,
-                "flops_per_launch": kf[dom], "mean_launch_us": round(per_kernel_ms[dom] * 1e3, 2)}
+                "flops_per_launch": kf[dom], "mean_launch_us": round(per_kernel_ms[dom] * 1e3, 2),
+                "timed_launches": len(ev)}
 
     line = {
         "metric": METRIC,
