@@ -54,6 +54,9 @@ template <int N> using IC = std::integral_constant<int, N>;
 #ifndef CATTN_BWD_SPLIT_WG_PER_CU  // backward at D = 64: split below this many unsplit workgroups per CU
 #define CATTN_BWD_SPLIT_WG_PER_CU 2
 #endif
+#ifndef CATTN_BAND  // rounds of work groups dealt in alternating directions (0: plain heaviest-first)
+#define CATTN_BAND cu_count()
+#endif
 #ifndef CATTN_DKDV_NB64S  // dQ and dK/dV at D = 64 with the loop range split in two (two rings)
 #define CATTN_DKDV_NB64S 4
 #endif
@@ -240,7 +243,7 @@ template <int D, bool CAUSAL, int SPLIT, int NB>
 __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                             const bf16* __restrict__ V, bf16* __restrict__ O,
                                                             float* __restrict__ LSE, int S, int BH, int n_qtiles,
-                                                            float c) {
+                                                            float c, int band) {
   typedef TileGeom<D> G;
   constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
   constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
@@ -253,7 +256,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   const int qg = w % QG, part = w / QG;
   int bh, qt;
-  tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
+  tile_of_block_banded(blockIdx.x, BH, n_qtiles, CAUSAL, CAUSAL ? band : 0, bh, qt);
   const int64_t base = (int64_t)bh * S * D;
   const bf16* Kb = K + base;
   const bf16* Vb = V + base;
@@ -477,7 +480,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
                                                                const bf16* __restrict__ dO,
                                                                const float* __restrict__ LSE, bf16* __restrict__ dQ,
                                                                float* __restrict__ ws, int S, int BH, int n_qtiles,
-                                                               float c, float scale) {
+                                                               float c, float scale, int band) {
   typedef TileGeom<D> G;
   constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
   constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
@@ -490,7 +493,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   const int qg = w % QG, part = w / QG;
   int bh, qt;
-  tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
+  tile_of_block_banded(blockIdx.x, BH, n_qtiles, CAUSAL, CAUSAL ? band : 0, bh, qt);
   const int64_t base = (int64_t)bh * S * D;
   const bf16* Kb = K + base;
   const bf16* Vb = V + base;
@@ -916,7 +919,7 @@ static hipError_t launch_dq(const BwdArgs& a, float c, hipStream_t st) {
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
-                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale);
+                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, CATTN_BAND);
   return hipGetLastError();
 }
 
@@ -936,7 +939,7 @@ static hipError_t launch_fwd_split(const FwdArgs& a, hipStream_t st) {
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S,
-                     a.BH, n_qtiles, a.scale * kLog2e);
+                     a.BH, n_qtiles, a.scale * kLog2e, CATTN_BAND);
   return hipGetLastError();
 }
 

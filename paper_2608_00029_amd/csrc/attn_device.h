@@ -20,6 +20,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "attn_sched.h"
+
 // Occupancy targets (waves per SIMD) handed to the register allocator.
 #ifndef CATTN_WPE_FWD
 #define CATTN_WPE_FWD 0
@@ -236,6 +238,13 @@ __device__ __forceinline__ void tile_of_block(int bid, int BH, int ntiles, bool 
   bh = bid % BH;
   const int t = bid / BH;
   tile = heavy_last ? (ntiles - 1 - t) : t;
+}
+// The same, with the heaviest-first ranks dealt to rounds of `band` work groups
+// in alternating directions (banded_rank), so that the work groups sharing a
+// compute unit carry complementary amounts of causal work.
+__device__ __forceinline__ void tile_of_block_banded(int bid, int BH, int ntiles, bool heavy_last, int band, int& bh,
+                                                     int& tile) {
+  tile_of_block(banded_rank(bid, BH * ntiles, band), BH, ntiles, heavy_last, bh, tile);
 }
 
 }  // namespace cattn

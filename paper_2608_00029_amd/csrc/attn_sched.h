@@ -30,4 +30,20 @@ constexpr int ring_in_flight(int i, int L, int n_last, int split, int ahead, int
 // (i + ahead - 1 < n_last): a compile-time count.
 constexpr int ring_in_flight_full(int split, int ahead, int need) { return (ahead - 1 - need) * split; }
 
+// Order in which a grid of n work groups takes the work items, when items are
+// ranked heaviest first (rank 0 = most work).  Work groups are placed on the
+// GPU in rounds of `band` (one per compute unit): group b shares its compute
+// unit with groups b +- band, b +- 2 band, ...  Every other round walks the
+// ranks backwards, so that a compute unit that receives one of the heaviest
+// items in one round receives one of the lightest of the next.  band <= 0
+// keeps the plain heaviest-first order.  A permutation of [0, n).
+constexpr int banded_rank(int bid, int n, int band) {
+  if (band <= 0) return bid;
+  const int r = bid / band, p = bid % band;
+  if ((r & 1) == 0) return bid;
+  const int size = n - r * band < band ? n - r * band : band;
+  return r * band + size - 1 - p;
+}
+
 }  // namespace cattn
+

@@ -42,6 +42,19 @@ int main() {
       }
     }
   }
+  // banded_rank is a permutation of [0, n) for every grid size and band
+  for (int n = 1; n <= 1200; n += 7) {
+    for (int band : {0, 1, 3, 80, 256, 304}) {
+      static unsigned char seen[1200];
+      for (int i = 0; i < n; ++i) seen[i] = 0;
+      for (int b = 0; b < n; ++b) {
+        ++checks;
+        const int r = banded_rank(b, n, band);
+        if (r < 0 || r >= n || seen[r]) ++bad;
+        else seen[r] = 1;
+      }
+    }
+  }
   for (int S = 1; S <= 5000; ++S) {
     const int p = ws_rows(S);
     if (p % 32 != 0 || p < S || p >= S + 32) ++bad;
