@@ -313,11 +313,18 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   f32x16 oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
-  // Pipeline state: sa = S(j); pp, vf = P(j-1) and V(j-1) for O += P V.
-  f32x16 sa = f32x16{};
-  MB::frag pp[2], vf[2][DT];
-  pp[0] = MB::frag{};
-  pp[1] = MB::frag{};
+  // Pipeline state of iteration j: sa = S(j); pp, vf = P(j-1) and V(j-1) for O += P V.
+  // With an even ring depth the two copies alternate by ring slot parity (every
+  // index a constant, no register moves); otherwise index 1 is copied to 0.
+  constexpr bool PAR = NB % 2 == 0;
+  f32x16 sa[2];
+  MB::frag pp[2][2], vf[2][DT];  // V(j-1) is read into the same registers once O += P V has issued
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    sa[x] = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) pp[x][ks] = MB::frag{};
+  }
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -326,7 +333,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
     MB::frag k0f[KS_D];
     read_rows<D>(ring, r, h, k0f);
 #pragma unroll
-    for (int ks = 0; ks < KS_D; ++ks) sa = MB::run(k0f[ks], qf[ks], sa);
+    for (int ks = 0; ks < KS_D; ++ks) sa[0] = MB::run(k0f[ks], qf[ks], sa[0]);
   }
 
   auto softmax = [&](const f32x16& s, float mc, f32x16& pv) {
@@ -343,6 +350,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   for (int i0 = 0; i0 < L; i0 += NB) {
     unroll<NB>([&](auto slc) {
       constexpr int sl = decltype(slc)::value;
+      constexpr int pc = PAR ? (sl & 1) : 0, pn = PAR ? (pc ^ 1) : 1;
       const int i = i0 + sl;
       if (i >= L) return;
       if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
@@ -354,13 +362,14 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       }
       if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
+      f32x16& sa_ = sa[pc];
       // causal diagonal / ragged end: only the last tile of the wave's queries
       if (i == i_mask) {
         const int k0 = (tb + i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int key = k0 + acc_row(a, h);
-          if (key >= S || (CAUSAL && key > my_q)) sa[a] = kMasked;
+          if (key >= S || (CAUSAL && key > my_q)) sa_[a] = kMasked;
         }
       }
       // K of the next tile.  On a wave's last iteration this slot holds another
@@ -369,18 +378,19 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       read_rows<D>(ring + ((sl + 1) % NB) * SET, r, h, kf);
       __builtin_amdgcn_sched_barrier(0);  // issue the K reads before anything below
       f32x16 pv;
-      float psum = softmax(sa, m * c, pv);
+      float psum = softmax(sa_, m * c, pv);
       // matrix cores, independent of the softmax: O += P(j-1) V(j-1), S(j+1) = K Q^T
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pp[ks], oacc[dt]);
-      f32x16 sn = f32x16{};
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pp[pc][ks], oacc[dt]);
+      f32x16& sn = sa[pn];
+      sn = f32x16{};
 #pragma unroll
       for (int ks = 0; ks < KS_D; ++ks) sn = MB::run(kf[ks], qf[ks], sn);
-      MB::frag pn[2];
+      MB::frag (&pn_)[2] = pp[pn];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) pn[ks] = MB::pack(pv, ks);
+      for (int ks = 0; ks < 2; ++ks) pn_[ks] = MB::pack(pv, ks);
 #pragma unroll
       for (int e = 0; e < 2 * DT + KS_D; ++e) {  // interleave matrix-core and vector work
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -388,36 +398,46 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       }
       // The new P and its sum are finished here, above the branch, so that
       // the exponentials stay in the same block as the contractions.
-      asm volatile("" ::"v"(psum), "v"(pn[0]), "v"(pn[1]));
+      asm volatile("" ::"v"(psum), "v"(pn_[0]), "v"(pn_[1]));
       read_trans<D>(ring + sl * SET + TILE, lane, vf);  // V(j), for the next iteration
       if (__builtin_amdgcn_ballot_w64(!(psum <= kSumMax))) {  // rare: move the offset
         // keeps this block a real branch: executed speculatively it would make
         // every iteration wait for the matrix-core accumulation above
         asm volatile("" ::: "memory");
-        float mx = sa[0];
+        float mx = sa_[0];
 #pragma unroll
-        for (int a = 1; a < 16; ++a) mx = fmaxf(mx, sa[a]);
+        for (int a = 1; a < 16; ++a) mx = fmaxf(mx, sa_[a]);
         const float mnew = fmaxf(m, halves_max(mx));  // same in both halves of a query
         const float alpha = exp2_hw((m - mnew) * c);  // 0 on the first block
         m = mnew;
-        psum = softmax(sa, m * c, pv);
+        psum = softmax(sa_, m * c, pv);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) pn[ks] = MB::pack(pv, ks);
+        for (int ks = 0; ks < 2; ++ks) pn_[ks] = MB::pack(pv, ks);
         lsum *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;  // after O += P(j-1) V(j-1)
       }
       lsum += psum;
-      pp[0] = pn[0];
-      pp[1] = pn[1];
-      sa = sn;
+      if constexpr (!PAR) {
+        sa[0] = sa[1];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) pp[0][ks] = pp[1][ks];
+      }
     });
   }
-  if (cnt > 0) {  // drain: O += P(last) V(last)
+  // drain: O += P(last) V(last), held at index (cnt & 1) by parity (index 0 otherwise)
+  auto drain = [&](const MB::frag (&pl)[2]) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pp[ks], oacc[dt]);
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pl[ks], oacc[dt]);
+  };
+  if (cnt > 0) {
+    if (PAR && (cnt & 1)) {
+      drain(pp[1]);
+    } else {
+      drain(pp[0]);
+    }
   }
 
   if constexpr (SPLIT == 2) {
