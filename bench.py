@@ -11,8 +11,10 @@ The same timed region also records HIP events around each kernel, on the
 stream the kernels run on, on every 8th step (--event-every); the slowest
 kernel's mean duration over those launches gives the roofline entry.  After
 the timed region every workload (the tiny float32 one, GPT-2 small/medium, XL
-width, long context) is timed too -- forward, backward and whole step -- under
-"configs" (--configs 0 skips it; profile runs do).  On
+width, long context, and GPT-2 small stored [B, S, H, D]) is timed too --
+forward, backward and whole step -- under "configs", and shapes across the
+paper's attention sweep under "sweep" (--configs 0 skips both; profile runs
+do).  On
 rank 0 the float64 CPU oracle is then timed on a bounded sample of the same
 workload (whole (batch, head) slices) as a reported baseline.  Prints ONE JSON
 line.
@@ -118,30 +120,34 @@ def cpu_baseline(w, inputs, budget_s: float):
                       f"{dt:.1f} s wall"}
 
 
-def time_workload(w, bd, steps: int, warmup: int):
+def time_workload(w, bd, steps: int, warmup: int, layout: str = "bhsd"):
     """Forward, backward (dQ then dK/dV) and whole-step times of one workload,
     inputs resident in HBM: mean ms over `steps` launches of each, timed with
-    HIP events on the stream the kernels run on."""
+    HIP events on the stream the kernels run on.  layout "bshd" stores the
+    tensors [B, S, H, D] (read and written in place by the kernels)."""
     import ctypes
     import torch
     from paper_2608_00029_amd.workloads import workload_inputs
     dev = torch.device("cuda:0")
     q, k, v, do = (t.to(dev) for t in workload_inputs(w))
+    if layout == "bshd":
+        q, k, v, do = (t.transpose(1, 2).contiguous() for t in (q, k, v, do))
     o = torch.empty_like(q)
     lse = torch.empty((w.B, w.H, w.S), dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
     ws = torch.empty((bd.workspace_bytes(w.B, w.H, w.S, w.D) // 4,), dtype=torch.float32, device=dev)
     L = bd.lib()
     stream = torch.cuda.current_stream(dev)
+    lay = bd.CATTN_BSHD if layout == "bshd" else bd.CATTN_BHSD
     shape = (w.B, w.H, w.S, w.D, float(w.scale), int(w.causal), bd.CATTN_BF16 if w.dtype == "bf16" else bd.CATTN_F32,
-             ctypes.c_void_p(stream.cuda_stream))
+             lay, ctypes.c_void_p(stream.cuda_stream))
     P = lambda t: t.data_ptr()  # noqa: E731
 
     def fwd():
-        return L.cattn_attn_fwd(P(q), P(k), P(v), P(o), P(lse), *shape)
+        return L.cattn_attn_fwd_ex(P(q), P(k), P(v), P(o), P(lse), *shape)
 
     def bwd():
-        return L.cattn_attn_bwd(P(q), P(k), P(v), P(o), P(do), P(lse), P(dq), P(dk), P(dv), P(ws), *shape)
+        return L.cattn_attn_bwd_ex(P(q), P(k), P(v), P(o), P(do), P(lse), P(dq), P(dk), P(dv), P(ws), *shape)
 
     for _ in range(warmup):
         if fwd() != 0 or bwd() != 0:
@@ -299,8 +305,10 @@ def main() -> int:
         "roofline": roofline,
     }
     if args.configs:
-        from paper_2608_00029_amd.workloads import WORKLOADS
+        from paper_2608_00029_amd.workloads import SWEEP, WORKLOADS
         line["configs"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in WORKLOADS}
+        line["configs"][w.name + "_bshd"] = time_workload(w, bd, steps=20, warmup=5, layout="bshd")
+        line["sweep"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in SWEEP}
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, cpu_inputs, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -73,6 +73,19 @@ typedef enum {
   CATTN_BF16 = 1
 } cattn_dtype;
 
+/* Storage order of Q, K, V, O, dO, dQ, dK, dV (LSE and the workspace are
+ * [B, H, S] in both).  CATTN_BHSD: contiguous [B, H, S, D], one head's S x D
+ * matrix contiguous.  CATTN_BSHD: contiguous [B, S, H, D], the order a
+ * query/key/value projection of a [B, S, H*D] activation produces before the
+ * usual head-major repack.  Section 4.2 (building the online softmax) absorbs
+ * that repack into how the attention operator indexes its operands instead of
+ * running transpose kernels; here the kernels likewise read and write
+ * [B, S, H, D] in place (rows of one head H*D elements apart). */
+typedef enum {
+  CATTN_BHSD = 0,
+  CATTN_BSHD = 1
+} cattn_layout;
+
 /*
  * Forward pass (section 4.2: online softmax over key tiles, base-2 exponent
  * with the scale folded in, finite mask sentinel, causal loop clamping, LSE
@@ -112,6 +125,24 @@ cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v,
                             void* dq, void* dk, void* dv, float* workspace,
                             int B, int H, int S, int D,
                             float scale, int causal, int dtype, void* stream);
+
+/*
+ * cattn_attn_fwd and cattn_attn_bwd with an explicit storage order `layout`
+ * (cattn_layout) of the [.., D] tensors; everything else -- arguments,
+ * sizes, the LSE and workspace layouts, error behaviour -- is as above.  An
+ * unknown layout is CATTN_ERR_INVALID_ARG.  cattn_attn_fwd(...) is
+ * cattn_attn_fwd_ex(..., CATTN_BHSD, stream), and likewise for the backward.
+ */
+cattn_status cattn_attn_fwd_ex(const void* q, const void* k, const void* v,
+                               void* o, float* lse,
+                               int B, int H, int S, int D,
+                               float scale, int causal, int dtype, int layout, void* stream);
+
+cattn_status cattn_attn_bwd_ex(const void* q, const void* k, const void* v,
+                               const void* o, const void* dout, const float* lse,
+                               void* dq, void* dk, void* dv, float* workspace,
+                               int B, int H, int S, int D,
+                               float scale, int causal, int dtype, int layout, void* stream);
 
 /*
  * The two phases of cattn_attn_bwd as separate calls, for callers that

@@ -21,7 +21,11 @@ _lib: Optional[ctypes.CDLL] = None
 CATTN_OK, CATTN_ERR_INVALID_ARG, CATTN_ERR_UNSUPPORTED, CATTN_ERR_HIP = 0, 1, 2, 3
 CATTN_F32, CATTN_BF16 = 0, 1
 
-EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_attn_bwd_dq", "cattn_attn_bwd_dkdv",
+CATTN_BHSD, CATTN_BSHD = 0, 1
+_LAYOUTS = {"bhsd": CATTN_BHSD, "bshd": CATTN_BSHD}
+
+EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_attn_fwd_ex", "cattn_attn_bwd_ex", "cattn_attn_bwd_dq",
+            "cattn_attn_bwd_dkdv",
             "cattn_bwd_workspace_bytes", "cattn_status_string", "cattn_last_error_string")
 
 
@@ -48,6 +52,10 @@ def lib() -> ctypes.CDLL:
         L.cattn_attn_fwd.restype = i
         L.cattn_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
         L.cattn_attn_bwd.restype = i
+        L.cattn_attn_fwd_ex.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, f, i, i, i, vp]
+        L.cattn_attn_fwd_ex.restype = i
+        L.cattn_attn_bwd_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, i, vp]
+        L.cattn_attn_bwd_ex.restype = i
         L.cattn_attn_bwd_dq.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
         L.cattn_attn_bwd_dq.restype = i
         L.cattn_attn_bwd_dkdv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
@@ -103,15 +111,28 @@ def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def attn_fwd(q, k, v, scale: float, causal: bool = True, o=None, lse=None):
-    """O, LSE = attention forward of contiguous [B, H, S, D] tensors on a HIP device.
-
-    LSE is float32 [B, H, S] in natural-log units.  `o` / `lse` may be passed
-    to write into existing buffers.  Enqueued on torch's current stream.
-    """
+def _shape(q, layout: str):
+    """(B, H, S, D) of a contiguous 4-d tensor stored in `layout` ("bhsd" or "bshd")."""
+    if layout not in _LAYOUTS:
+        raise ValueError(f"layout must be 'bhsd' or 'bshd', not {layout!r}")
     if q.dim() != 4:
-        raise ValueError("q must be [B, H, S, D]")
-    B, H, S, D = q.shape
+        raise ValueError(f"q must be 4-d ({layout.upper()})")
+    if layout == "bhsd":
+        B, H, S, D = q.shape
+    else:
+        B, S, H, D = q.shape
+    return B, H, S, D
+
+
+def attn_fwd(q, k, v, scale: float, causal: bool = True, o=None, lse=None, layout: str = "bhsd"):
+    """O, LSE = attention forward of contiguous tensors on a HIP device.
+
+    Q, K, V (and O) are [B, H, S, D] for layout "bhsd", [B, S, H, D] for
+    "bshd" (read and written in place, no transposes).  LSE is float32
+    [B, H, S] in natural-log units in both.  `o` / `lse` may be passed to
+    write into existing buffers.  Enqueued on torch's current stream.
+    """
+    B, H, S, D = _shape(q, layout)
     if q.device.type != "cuda":
         raise ValueError("tensors must live on a HIP device")
     for n, t in (("q", q), ("k", k), ("v", v)):
@@ -122,23 +143,22 @@ def attn_fwd(q, k, v, scale: float, causal: bool = True, o=None, lse=None):
         lse = torch.empty((B, H, S), dtype=torch.float32, device=q.device)
     _check("o", o, q.shape, q.dtype, q.device)
     _check("lse", lse, (B, H, S), torch.float32, q.device)
-    st = lib().cattn_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, S, D, float(scale),
-                              int(bool(causal)), _dtype_code(q), _stream(q.device))
+    st = lib().cattn_attn_fwd_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, S, D, float(scale),
+                                 int(bool(causal)), _dtype_code(q), _LAYOUTS[layout], _stream(q.device))
     if st != CATTN_OK:
-        raise CattnError(st, "cattn_attn_fwd", last_error_string())
+        raise CattnError(st, "cattn_attn_fwd_ex", last_error_string())
     return o, lse
 
 
 def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk=None, dv=None,
-             workspace=None):
+             workspace=None, layout: str = "bhsd"):
     """dQ, dK, dV of attention for upstream gradient `do`, given the forward's O and LSE.
 
-    `workspace` (float32, >= workspace_bytes(B, H, S, D) / 4 elements) receives D = rowsum(dO * O)
-    and LSE * log2(e), each [B*H, S rounded up to 32] with zero padding rows.
+    Tensors are stored as for attn_fwd with the same `layout`.  `workspace` (float32,
+    >= workspace_bytes(B, H, S, D) / 4 elements) receives D = rowsum(dO * O) and
+    -LSE / scale, each [B*H, S rounded up to 32] with zero padding rows.
     """
-    if q.dim() != 4:
-        raise ValueError("q must be [B, H, S, D]")
-    B, H, S, D = q.shape
+    B, H, S, D = _shape(q, layout)
     if q.device.type != "cuda":
         raise ValueError("tensors must live on a HIP device")
     for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do)):
@@ -153,11 +173,11 @@ def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk
     if workspace is None:
         workspace = torch.empty((nws,), dtype=torch.float32, device=q.device)
     _check_workspace(workspace, nws, q.device)
-    st = lib().cattn_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq), _ptr(dk),
-                              _ptr(dv), _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)),
-                              _dtype_code(q), _stream(q.device))
+    st = lib().cattn_attn_bwd_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq), _ptr(dk),
+                                 _ptr(dv), _ptr(workspace), B, H, S, D, float(scale), int(bool(causal)),
+                                 _dtype_code(q), _LAYOUTS[layout], _stream(q.device))
     if st != CATTN_OK:
-        raise CattnError(st, "cattn_attn_bwd", last_error_string())
+        raise CattnError(st, "cattn_attn_bwd_ex", last_error_string())
     return dq, dk, dv
 
 

@@ -146,7 +146,7 @@ __device__ __forceinline__ void dma16(const void* sbase, unsigned voff, unsigned
 }
 #pragma clang diagnostic pop
 
-// HBM -> LDS copy of 32-row tiles of a row-major [S][D] bf16 tensor.  The
+// HBM -> LDS copy of 32-row tiles of an [S][D] bf16 matrix whose rows are rs elements apart.  The
 // chunk a lane deposits at physical position p of the tile is logical chunk
 // p ^ swz(row), so the LDS image has the swizzled layout Tile<> reads.  The
 // per-lane source offsets inside a tile are fixed for the kernel; only the
@@ -154,26 +154,27 @@ __device__ __forceinline__ void dma16(const void* sbase, unsigned voff, unsigned
 template <int D> struct TileCopy {
   typedef TileGeom<D> G;
   unsigned voff[G::DMA_PER_TENSOR];
-  int w, lane;
-  __device__ __forceinline__ void init(int w_, int lane_) {
+  int w, lane, rs;
+  __device__ __forceinline__ void init(int w_, int lane_, int rs_) {
     w = w_;
     lane = lane_;
+    rs = rs_;
 #pragma unroll
     for (int i = 0; i < G::DMA_PER_TENSOR; ++i) {
       const int p = i * 256 + w * 64 + lane;
       const int row = p / G::CPR;
-      voff[i] = (unsigned)(row * D * 2 + (((p % G::CPR) ^ swz(row)) << 4));
+      voff[i] = (unsigned)(row * rs * 2 + (((p % G::CPR) ^ swz(row)) << 4));
     }
   }
   // a tile known to lie inside the sequence (row0 + 32 <= nrows)
   __device__ __forceinline__ void copy_full(const bf16* g, int row0, char* lds) const {
-    const bf16* src = g + (int64_t)row0 * D;
+    const bf16* src = g + (int64_t)row0 * rs;
     const unsigned dst = lds_addr(lds) + w * 64 * 16;
 #pragma unroll
     for (int i = 0; i < G::DMA_PER_TENSOR; ++i) dma16(src, voff[i], dst + i * 256 * 16);
   }
   __device__ __forceinline__ void copy(const bf16* g, int row0, int nrows, char* lds) const {
-    const bf16* src = g + (int64_t)row0 * D;
+    const bf16* src = g + (int64_t)row0 * rs;
     const unsigned dst = lds_addr(lds) + w * 64 * 16;
     if (row0 + 32 <= nrows) {
 #pragma unroll
@@ -184,7 +185,7 @@ template <int D> struct TileCopy {
         const int p = i * 256 + w * 64 + lane;
         const int row = p / G::CPR, lc = (p % G::CPR) ^ swz(row);
         const int src_row = min(row, nrows - 1 - row0);
-        dma16(src, (unsigned)(src_row * D * 2 + lc * 16), dst + i * 256 * 16);
+        dma16(src, (unsigned)(src_row * rs * 2 + lc * 16), dst + i * 256 * 16);
       }
     }
   }
@@ -243,7 +244,7 @@ template <int D, bool CAUSAL, int SPLIT, int NB>
 __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                             const bf16* __restrict__ V, bf16* __restrict__ O,
                                                             float* __restrict__ LSE, int S, int BH, int n_qtiles,
-                                                            float c, int band) {
+                                                            float c, int band, int H, int seq_major) {
   typedef TileGeom<D> G;
   constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
   constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
@@ -257,7 +258,9 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const int qg = w % QG, part = w / QG;
   int bh, qt;
   tile_of_block_banded(blockIdx.x, BH, n_qtiles, CAUSAL, CAUSAL ? band : 0, bh, qt);
-  const int64_t base = (int64_t)bh * S * D;
+  const Rows rw = rows_of(bh, H, S, D, seq_major);
+  const int64_t base = rw.base;
+  const int rs = rw.rs;
   const bf16* Kb = K + base;
   const bf16* Vb = V + base;
 
@@ -279,7 +282,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const int i_mask = nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
 
   TileCopy<D> tc;
-  tc.init(w, lane);
+  tc.init(w, lane, rs);
   const char* ring = smem + part * NB * SET;  // this wave's part
   auto dma = [&](int x, auto slc) {  // iteration x's tile of every part, into ring slot slc
 #pragma unroll
@@ -305,7 +308,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
     if (decltype(I)::value < L) dma(decltype(I)::value, I);
   });
   MB::frag qf[KS_D];
-  load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
+  load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
   wait_vm(0);
   __syncthreads();
 
@@ -470,7 +473,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const float l = halves_sum(lsum);
   if (my_q < S) {
     const float inv = 1.0f / l;
-    bf16* orow = O + base + (int64_t)my_q * D;
+    bf16* orow = O + base + (int64_t)my_q * rs;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -500,7 +503,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
                                                                const bf16* __restrict__ dO,
                                                                const float* __restrict__ LSE, bf16* __restrict__ dQ,
                                                                float* __restrict__ ws, int S, int BH, int n_qtiles,
-                                                               float c, float scale, int band) {
+                                                               float c, float scale, int band, int H, int seq_major) {
   typedef TileGeom<D> G;
   constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
   constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
@@ -514,7 +517,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int qg = w % QG, part = w / QG;
   int bh, qt;
   tile_of_block_banded(blockIdx.x, BH, n_qtiles, CAUSAL, CAUSAL ? band : 0, bh, qt);
-  const int64_t base = (int64_t)bh * S * D;
+  const Rows rw = rows_of(bh, H, S, D, seq_major);
+  const int64_t base = rw.base;
+  const int rs = rw.rs;
   const bf16* Kb = K + base;
   const bf16* Vb = V + base;
   const int Sp = ws_rows(S);
@@ -537,7 +542,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int i_mask = nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
 
   TileCopy<D> tc;
-  tc.init(w, lane);
+  tc.init(w, lane, rs);
   auto dma = [&](int x, auto slc) {  // iteration x's tile of every part, into ring slot slc
 #pragma unroll
     for (int p = 0; p < SPLIT; ++p) {
@@ -561,9 +566,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
     if (decltype(I)::value < L) dma(decltype(I)::value, I);
   });
   MB::frag qf[KS_D], dof[KS_D], of[KS_D];
-  load_row_frags<bf16, D>(Q + base, my_q, S, h, qf);
-  load_row_frags<bf16, D>(dO + base, my_q, S, h, dof);
-  load_row_frags<bf16, D>(O + base, my_q, S, h, of);
+  load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
+  load_row_frags<bf16, D>(dO + base, my_q, S, h, rs, dof);
+  load_row_frags<bf16, D>(O + base, my_q, S, h, rs, of);
   const float lse = my_q < S ? LSE[(int64_t)bh * S + my_q] : 0.f;
   wait_vm(0);
   __syncthreads();
@@ -664,7 +669,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   }
 
   if (my_q < S) {
-    bf16* row = dQ + base + (int64_t)my_q * D;
+    bf16* row = dQ + base + (int64_t)my_q * rs;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -700,7 +705,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
                                                                  const bf16* __restrict__ dO,
                                                                  const float* __restrict__ ws,
                                                                  bf16* __restrict__ dK, bf16* __restrict__ dV, int S,
-                                                                 int BH, int n_ktiles, float c, float scale) {
+                                                                 int BH, int n_ktiles, float c, float scale, int H,
+                                                                 int seq_major) {
   typedef TileGeom<D> G;
   constexpr int KG = 4 / SPLIT, BKV = 32 * KG;
   constexpr int AH = NB - 1, TILE = G::TILE;
@@ -716,7 +722,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const int kg = w % KG, part = w / KG;
   int bh, kt;
   tile_of_block(blockIdx.x, BH, n_ktiles, false, bh, kt);
-  const int64_t base = (int64_t)bh * S * D;
+  const Rows rw = rows_of(bh, H, S, D, seq_major);
+  const int64_t base = rw.base;
+  const int rs = rw.rs;
   const bf16* Qb = Q + base;
   const bf16* dOb = dO + base;
   const int Sp = ws_rows(S);
@@ -747,7 +755,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const int x_full = n_last;  // iterations below this have a tile in every part
 
   TileCopy<D> tc;
-  tc.init(w, lane);
+  tc.init(w, lane, rs);
   auto dma = [&](int x, auto slc) {  // iteration x's tile of every part, into ring slot slc
 #pragma unroll
     for (int p = 0; p < SPLIT; ++p) {
@@ -773,8 +781,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
     if (decltype(I)::value < L) dma(decltype(I)::value, I);
   });
   MB::frag kf[KS_D], vf[KS_D];
-  load_row_frags<bf16, D>(K + base, my_k, S, h, kf);
-  load_row_frags<bf16, D>(V + base, my_k, S, h, vf);
+  load_row_frags<bf16, D>(K + base, my_k, S, h, rs, kf);
+  load_row_frags<bf16, D>(V + base, my_k, S, h, rs, vf);
   wait_vm(0);
   __syncthreads();
 #pragma unroll
@@ -893,8 +901,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   }
 
   if (my_k < S) {
-    bf16* krow = dK + base + (int64_t)my_k * D;
-    bf16* vrow = dV + base + (int64_t)my_k * D;
+    bf16* krow = dK + base + (int64_t)my_k * rs;
+    bf16* vrow = dV + base + (int64_t)my_k * rs;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -939,7 +947,8 @@ static hipError_t launch_dq(const BwdArgs& a, float c, hipStream_t st) {
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
-                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, CATTN_BAND);
+                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, CATTN_BAND, a.H,
+                     (int)a.seq_major);
   return hipGetLastError();
 }
 
@@ -949,7 +958,7 @@ static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
   const int n_ktiles = (a.S + BKV - 1) / BKV;
   hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
-                     (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale);
+                     (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 
@@ -959,7 +968,7 @@ static hipError_t launch_fwd_split(const FwdArgs& a, hipStream_t st) {
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S,
-                     a.BH, n_qtiles, a.scale * kLog2e, CATTN_BAND);
+                     a.BH, n_qtiles, a.scale * kLog2e, CATTN_BAND, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 

@@ -34,7 +34,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
                                                           const T* __restrict__ V, const T* __restrict__ O,
                                                           const T* __restrict__ dO, const float* __restrict__ LSE,
                                                           T* __restrict__ dQ, float* __restrict__ Dvec, int S,
-                                                          int BH, int n_qtiles, float c, float scale) {
+                                                          int BH, int n_qtiles, float c, float scale, int H,
+                                                          int seq_major) {
   typedef Mma<T> M;
   constexpr int BQ = 128, BK = 64, NT = 256;
   constexpr int KS_D = D / M::K, KS_32 = 32 / M::K, DT = D / 32;
@@ -45,20 +46,22 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   int bh, qt;
   tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
-  const int64_t base = (int64_t)bh * S * D;
+  const Rows rw = rows_of(bh, H, S, D, seq_major);
+  const int64_t base = rw.base;
+  const int rs = rw.rs;
   const T* Kb = K + base;
   const T* Vb = V + base;
 
   const int q0 = qt * BQ, qw = q0 + 32 * w, my_q = qw + r;
   typename M::frag qf[KS_D], dof[KS_D];
-  load_row_frags<T, D>(Q + base, my_q, S, h, qf);
-  load_row_frags<T, D>(dO + base, my_q, S, h, dof);
+  load_row_frags<T, D>(Q + base, my_q, S, h, rs, qf);
+  load_row_frags<T, D>(dO + base, my_q, S, h, rs, dof);
 
   // D = rowsum(dO * O) in float, from the O the forward produced.
   float dpart = 0.f;
   {
     typename M::frag of[KS_D];
-    load_row_frags<T, D>(O + base, my_q, S, h, of);
+    load_row_frags<T, D>(O + base, my_q, S, h, rs, of);
 #pragma unroll
     for (int ks = 0; ks < KS_D; ++ks) {
       if constexpr (M::KL == 1) {
@@ -86,8 +89,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
 
   TileStage<T, D, BK, NT> sk, sv;
-  sk.load(Kb, 0, S, tid);
-  sv.load(Vb, 0, S, tid);
+  sk.load(Kb, 0, S, tid, rs);
+  sv.load(Vb, 0, S, tid, rs);
   sk.store(smem, tid);
   sv.store(smem + TILE, tid);
   __syncthreads();
@@ -95,8 +98,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   for (int kt = 0; kt < n_kt; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < n_kt) {
-      sk.load(Kb, (kt + 1) * BK, S, tid);
-      sv.load(Vb, (kt + 1) * BK, S, tid);
+      sk.load(Kb, (kt + 1) * BK, S, tid, rs);
+      sv.load(Vb, (kt + 1) * BK, S, tid, rs);
     }
     const char* lk = smem + buf * 2 * TILE;
     const char* lv = lk + TILE;
@@ -139,7 +142,7 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
   }
 
   if (my_q < S) {
-    T* row = dQ + base + (int64_t)my_q * D;
+    T* row = dQ + base + (int64_t)my_q * rs;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -155,7 +158,7 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
                                                             const float* __restrict__ LSE,
                                                             const float* __restrict__ Dvec, T* __restrict__ dK,
                                                             T* __restrict__ dV, int S, int BH, int n_ktiles,
-                                                            float c, float scale) {
+                                                            float c, float scale, int H, int seq_major) {
   typedef Mma<T> M;
   constexpr int BKV = 128, BQ = 64, NT = 256;
   constexpr int KS_D = D / M::K, KS_32 = 32 / M::K, DT = D / 32;
@@ -168,7 +171,9 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   int bh, kt;
   tile_of_block(blockIdx.x, BH, n_ktiles, false, bh, kt);
-  const int64_t base = (int64_t)bh * S * D;
+  const Rows rw = rows_of(bh, H, S, D, seq_major);
+  const int64_t base = rw.base;
+  const int rs = rw.rs;
   const T* Qb = Q + base;
   const T* dOb = dO + base;
   const float* Lb = LSE + (int64_t)bh * S;
@@ -176,8 +181,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
 
   const int k0 = kt * BKV, kw = k0 + 32 * w, my_k = kw + r;
   typename M::frag kf[KS_D], vf[KS_D];
-  load_row_frags<T, D>(K + base, my_k, S, h, kf);
-  load_row_frags<T, D>(V + base, my_k, S, h, vf);
+  load_row_frags<T, D>(K + base, my_k, S, h, rs, kf);
+  load_row_frags<T, D>(V + base, my_k, S, h, rs, vf);
 
   const int qstart = CAUSAL ? k0 : 0;  // causal: the query loop starts at the diagonal
   const int qt0 = qstart / BQ;
@@ -192,8 +197,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
   TileStage<T, D, BQ, NT> sq, sdo;
   float vec = 0.f;  // threads 0..63 stage LSE*log2e, threads 64..127 stage D
   auto load_tile = [&](int qt) {
-    sq.load(Qb, qt * BQ, S, tid);
-    sdo.load(dOb, qt * BQ, S, tid);
+    sq.load(Qb, qt * BQ, S, tid, rs);
+    sdo.load(dOb, qt * BQ, S, tid, rs);
     const int row = qt * BQ + (tid & 63);
     vec = 0.f;
     if (tid < 64) {
@@ -268,8 +273,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_d
   }
 
   if (my_k < S) {
-    T* krow = dK + base + (int64_t)my_k * D;
-    T* vrow = dV + base + (int64_t)my_k * D;
+    T* krow = dK + base + (int64_t)my_k * rs;
+    T* vrow = dV + base + (int64_t)my_k * rs;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -289,14 +294,14 @@ static hipError_t launch_bwd_t(const BwdArgs& a, int phase, hipStream_t st) {
     const int n_qtiles = (a.S + 127) / 128;
     hipLaunchKernelGGL((attn_bwd_dq_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256),
                        0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.o, (const T*)a.dout, a.lse,
-                       (T*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale);
+                       (T*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, a.H, (int)a.seq_major);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || phase == 1) return e;
   }
   const int n_ktiles = (a.S + 127) / 128;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, D, CAUSAL>), dim3((unsigned)((int64_t)a.BH * n_ktiles)), dim3(256),
                      0, st, (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, a.lse, a.ws,
-                     (T*)a.dk, (T*)a.dv, a.S, a.BH, n_ktiles, c, a.scale);
+                     (T*)a.dk, (T*)a.dv, a.S, a.BH, n_ktiles, c, a.scale, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 

@@ -163,13 +163,14 @@ template <typename T, int D, int R, int NT> struct TileStage {
   static_assert(R * kChunksPerRow % NT == 0, "tile must split evenly over the threads");
   u32x4 reg[kPerThread];
 
-  __device__ __forceinline__ void load(const T* g, int row0, int nrows, int tid) {
+  // rows of g are rs elements apart
+  __device__ __forceinline__ void load(const T* g, int row0, int nrows, int tid, int rs) {
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i) {
       const int c = tid + i * NT;
       const int row = c / kChunksPerRow, ch = c % kChunksPerRow;
       if (row0 + row < nrows) {
-        reg[i] = *(const u32x4*)((const char*)g + (int64_t)(row0 + row) * Tile<T, D>::kRowBytes + ch * 16);
+        reg[i] = *(const u32x4*)((const char*)g + ((int64_t)(row0 + row) * rs) * (int64_t)sizeof(T) + ch * 16);
       } else {
         reg[i] = u32x4{0u, 0u, 0u, 0u};
       }
@@ -214,19 +215,33 @@ template <> __device__ __forceinline__ void store4<__bf16>(__bf16* dst, float a,
 }
 
 // Load the contiguous-K B-operand fragments of one row straight from global
-// memory (zero when row >= S).
+// memory (zero when row >= S); rows of g are rs elements apart.
 template <typename T, int D>
-__device__ __forceinline__ void load_row_frags(const T* g, int row, int S, int h,
+__device__ __forceinline__ void load_row_frags(const T* g, int row, int S, int h, int rs,
                                                typename Mma<T>::frag (&f)[D / Mma<T>::K]) {
   typedef Mma<T> M;
 #pragma unroll
   for (int ks = 0; ks < D / M::K; ++ks) {
     if (row < S) {
-      f[ks] = *(const typename M::frag*)(g + (int64_t)row * D + ks * M::K + h * M::KL);
+      f[ks] = *(const typename M::frag*)(g + (int64_t)row * rs + ks * M::K + h * M::KL);
     } else {
       f[ks] = typename M::frag{};
     }
   }
+}
+
+// Where the S x D matrix of (batch, head) bh starts, in elements, and how far
+// apart its rows are: [B, H, S, D] storage (heads-major: rows D apart) or
+// [B, S, H, D] storage (sequence-major, the layout a fused QKV projection
+// produces: rows H*D apart, heads D apart).  Batch stride H*S*D in both.
+struct Rows {
+  int64_t base;
+  int rs;
+};
+__device__ __forceinline__ Rows rows_of(int bh, int H, int S, int D, bool seq_major) {
+  if (!seq_major) return Rows{(int64_t)bh * S * D, D};
+  const int b = bh / H, hh = bh - b * H;
+  return Rows{(int64_t)b * H * S * D + (int64_t)hh * D, H * D};
 }
 
 // Map a block index to (head, tile) so that the heaviest causal tiles start

@@ -22,7 +22,7 @@ template <typename T, int D, bool CAUSAL>
 __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                        const T* __restrict__ V, T* __restrict__ O,
                                                        float* __restrict__ LSE, int S, int BH, int n_qtiles,
-                                                       float c) {
+                                                       float c, int H, int seq_major) {
   typedef Mma<T> M;
   constexpr int BQ = 128, BK = 64, NT = 256;
   constexpr int KS_D = D / M::K;      // k-steps over the head dimension
@@ -35,14 +35,16 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_ke
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   int bh, qt;
   tile_of_block(blockIdx.x, BH, n_qtiles, CAUSAL, bh, qt);
-  const int64_t base = (int64_t)bh * S * D;
+  const Rows rw = rows_of(bh, H, S, D, seq_major);
+  const int64_t base = rw.base;
+  const int rs = rw.rs;
   const T* Qb = Q + base;
   const T* Kb = K + base;
   const T* Vb = V + base;
 
   const int q0 = qt * BQ, qw = q0 + 32 * w, my_q = qw + r;
   typename M::frag qf[KS_D];
-  load_row_frags<T, D>(Qb, my_q, S, h, qf);
+  load_row_frags<T, D>(Qb, my_q, S, h, rs, qf);
 
   const int kend = CAUSAL ? min(S, q0 + BQ) : S;  // causal loop clamping
   const int n_kt = (kend + BK - 1) / BK;
@@ -54,8 +56,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_ke
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
 
   TileStage<T, D, BK, NT> sk, sv;
-  sk.load(Kb, 0, S, tid);
-  sv.load(Vb, 0, S, tid);
+  sk.load(Kb, 0, S, tid, rs);
+  sv.load(Vb, 0, S, tid, rs);
   sk.store(smem, tid);
   sv.store(smem + TILE, tid);
   __syncthreads();
@@ -63,8 +65,8 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_ke
   for (int kt = 0; kt < n_kt; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < n_kt) {
-      sk.load(Kb, (kt + 1) * BK, S, tid);
-      sv.load(Vb, (kt + 1) * BK, S, tid);
+      sk.load(Kb, (kt + 1) * BK, S, tid, rs);
+      sv.load(Vb, (kt + 1) * BK, S, tid, rs);
     }
     const char* lk = smem + buf * 2 * TILE;
     const char* lv = lk + TILE;
@@ -128,7 +130,7 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_ke
   const float l = halves_sum(lsum);
   if (my_q < S) {
     const float inv = 1.0f / l;
-    T* orow = O + base + (int64_t)my_q * D;
+    T* orow = O + base + (int64_t)my_q * rs;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -145,7 +147,7 @@ hipError_t launch_fwd_t(const FwdArgs& a, hipStream_t st) {
   const int64_t blocks = (int64_t)a.BH * n_qtiles;
   hipLaunchKernelGGL((attn_fwd_kernel<T, D, CAUSAL>), dim3((unsigned)blocks), dim3(256), 0, st,
                      (const T*)a.q, (const T*)a.k, (const T*)a.v, (T*)a.o, a.lse, a.S, a.BH, n_qtiles,
-                     a.scale * kLog2e);
+                     a.scale * kLog2e, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 

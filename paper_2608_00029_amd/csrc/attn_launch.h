@@ -20,6 +20,8 @@ struct FwdArgs {
   float scale;
   bool causal;
   bool bf16;
+  int H;           // heads (BH = B * H)
+  bool seq_major;  // tensors stored [B, S, H, D] instead of [B, H, S, D]
 };
 
 struct BwdArgs {
@@ -37,6 +39,8 @@ struct BwdArgs {
   float scale;
   bool causal;
   bool bf16;
+  int H;           // heads (BH = B * H)
+  bool seq_major;  // tensors stored [B, S, H, D] instead of [B, H, S, D]
 };
 
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);

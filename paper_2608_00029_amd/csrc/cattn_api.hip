@@ -63,9 +63,10 @@ cattn_status hip_status(hipError_t e) {
 
 extern "C" {
 
-cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S,
-                            int D, float scale, int causal, int dtype, void* stream) {
+cattn_status cattn_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S,
+                               int D, float scale, int causal, int dtype, int layout, void* stream) {
   g_last_error[0] = '\0';
+  if (layout != CATTN_BHSD && layout != CATTN_BSHD) return fail(CATTN_ERR_INVALID_ARG, "unknown layout");
   bool empty;
   cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
   if (st != CATTN_OK || empty) return st;
@@ -79,9 +80,14 @@ cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v, void* o
       if (overlap(out, in)) return fail(CATTN_ERR_INVALID_ARG, "an output overlaps an input");
   if (overlap(ro, rl)) return fail(CATTN_ERR_INVALID_ARG, "o overlaps lse");
 
-  cattn::FwdArgs a{q, k, v, o, lse, B * H, S, D, scale, causal != 0, dtype == CATTN_BF16};
+  cattn::FwdArgs a{q, k, v, o, lse, B * H, S, D, scale, causal != 0, dtype == CATTN_BF16, H, layout == CATTN_BSHD};
   (void)hipGetLastError();  // do not report an earlier, unrelated error as ours
   return hip_status(cattn::launch_fwd(a, (hipStream_t)stream));
+}
+
+cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S,
+                            int D, float scale, int causal, int dtype, void* stream) {
+  return cattn_attn_fwd_ex(q, k, v, o, lse, B, H, S, D, scale, causal, dtype, CATTN_BHSD, stream);
 }
 
 }  // extern "C"
@@ -93,8 +99,9 @@ namespace {
 // output of phases 0 and 1 and an input of phase 2.
 cattn_status bwd_common(const void* q, const void* k, const void* v, const void* o, const void* dout,
                         const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H, int S,
-                        int D, float scale, int causal, int dtype, void* stream, int phase) {
+                        int D, float scale, int causal, int dtype, int layout, void* stream, int phase) {
   g_last_error[0] = '\0';
+  if (layout != CATTN_BHSD && layout != CATTN_BSHD) return fail(CATTN_ERR_INVALID_ARG, "unknown layout");
   bool empty;
   cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
   if (st != CATTN_OK || empty) return st;
@@ -129,7 +136,7 @@ cattn_status bwd_common(const void* q, const void* k, const void* v, const void*
       if (overlap(outs[i], outs[j])) return fail(CATTN_ERR_INVALID_ARG, "outputs or workspace overlap each other");
 
   cattn::BwdArgs a{q, k, v, o, dout, lse, dq, dk, dv, workspace, B * H, S, D, scale, causal != 0,
-                   dtype == CATTN_BF16};
+                   dtype == CATTN_BF16, H, layout == CATTN_BSHD};
   (void)hipGetLastError();
   return hip_status(cattn::launch_bwd(a, phase, (hipStream_t)stream));
 }
@@ -141,21 +148,29 @@ extern "C" {
 cattn_status cattn_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
                             const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H, int S,
                             int D, float scale, int causal, int dtype, void* stream) {
-  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, workspace, B, H, S, D, scale, causal, dtype, stream, 0);
+  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, workspace, B, H, S, D, scale, causal, dtype, CATTN_BHSD,
+                    stream, 0);
+}
+
+cattn_status cattn_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                               const float* lse, void* dq, void* dk, void* dv, float* workspace, int B, int H,
+                               int S, int D, float scale, int causal, int dtype, int layout, void* stream) {
+  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, workspace, B, H, S, D, scale, causal, dtype, layout, stream,
+                    0);
 }
 
 cattn_status cattn_attn_bwd_dq(const void* q, const void* k, const void* v, const void* o, const void* dout,
                                const float* lse, void* dq, float* workspace, int B, int H, int S, int D,
                                float scale, int causal, int dtype, void* stream) {
   return bwd_common(q, k, v, o, dout, lse, dq, nullptr, nullptr, workspace, B, H, S, D, scale, causal, dtype,
-                    stream, 1);
+                    CATTN_BHSD, stream, 1);
 }
 
 cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout, const float* lse,
                                  const float* workspace, void* dk, void* dv, int B, int H, int S, int D,
                                  float scale, int causal, int dtype, void* stream) {
   return bwd_common(q, k, v, nullptr, dout, lse, nullptr, dk, dv, const_cast<float*>(workspace), B, H, S, D,
-                    scale, causal, dtype, stream, 2);
+                    scale, causal, dtype, CATTN_BHSD, stream, 2);
 }
 
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D) {

@@ -64,7 +64,23 @@ WORKLOADS = [
              SEED_BASE + 4),
 ]
 
-BY_NAME = {w.name: w for w in WORKLOADS}
+# Shapes of the kind the paper's attention sweep covers (sequence lengths 512,
+# 1024 and 2048, 12 to 32 heads, head dimension 64 or 128; section 6, attention
+# benchmark), at the batch of 16 its attention microbenchmark uses.  The paper
+# prints its per-shape results only as figures, so these are representative
+# points of that range, not its exact list; B16 H12 S1024 D64 is the shape of
+# its fused-attention latency figure.  Timed by the benchmark after its timed
+# region and parity-checked on sampled heads, like the workloads above.
+SWEEP = [
+    Workload("sweep_B16_H12_S512_D64", 16, 12, 512, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 10),
+    Workload("sweep_B16_H12_S1024_D64", 16, 12, 1024, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 11),
+    Workload("sweep_B16_H12_S2048_D64", 16, 12, 2048, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 12),
+    Workload("sweep_B16_H32_S1024_D64", 16, 32, 1024, 64, 1.0 / 8.0, "bf16", 1.0, SEED_BASE + 13),
+    Workload("sweep_B16_H16_S512_D128", 16, 16, 512, 128, 1.0 / math.sqrt(128.0), "bf16", 1.0, SEED_BASE + 14),
+    Workload("sweep_B16_H16_S1024_D128", 16, 16, 1024, 128, 1.0 / math.sqrt(128.0), "bf16", 1.0, SEED_BASE + 15),
+]
+
+BY_NAME = {w.name: w for w in WORKLOADS + SWEEP}
 
 
 def make_inputs(B: int, H: int, S: int, D: int, dtype: str = "bf16", seed: int = SEED_BASE,

@@ -116,3 +116,20 @@ def test_binding_refuses_cpu_tensors(lib):
     q = torch.zeros(1, 1, 8, 64)
     with pytest.raises(ValueError):
         b.attn_fwd(q, q, q, 0.125)
+
+
+def test_unknown_layout_is_rejected_before_any_launch(lib):
+    vp = __import__("ctypes").c_void_p
+    fake = [vp(4096 * (i + 1)) for i in range(10)]  # never dereferenced: the layout check comes first
+    for layout in (-1, 2, 7):
+        st = lib.cattn_attn_fwd_ex(*fake[:5], 1, 2, 64, 64, 0.125, 1, 1, layout, vp(0))
+        assert st == b.CATTN_ERR_INVALID_ARG
+        assert "layout" in b.last_error_string()
+        st = lib.cattn_attn_bwd_ex(*fake, 1, 2, 64, 64, 0.125, 1, 1, layout, vp(0))
+        assert st == b.CATTN_ERR_INVALID_ARG
+
+
+def test_empty_problem_in_either_layout_is_a_noop(lib):
+    vp = __import__("ctypes").c_void_p
+    for layout in (b.CATTN_BHSD, b.CATTN_BSHD):
+        assert lib.cattn_attn_fwd_ex(*[vp(0)] * 5, 0, 2, 64, 64, 0.125, 1, 1, layout, vp(0)) == b.CATTN_OK

@@ -16,7 +16,7 @@ import torch
 
 import oracle.attn_oracle as orc
 from paper_2608_00029_amd import attn_bwd, attn_fwd
-from paper_2608_00029_amd.workloads import WORKLOADS, make_inputs, workload_inputs
+from paper_2608_00029_amd.workloads import SWEEP, WORKLOADS, make_inputs, workload_inputs
 from parity_util import check_tensor, say, to64
 
 pytestmark = pytest.mark.gpu
@@ -95,7 +95,7 @@ def sampled_heads(B, H):
     return sorted({(0, 0), (B // 2, H // 2), (B - 1, H - 1)})
 
 
-@pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
+@pytest.mark.parametrize("w", WORKLOADS + SWEEP, ids=lambda w: w.name)
 def test_workload_parity(cuda, w):
     """Full-size run; every element of the sampled (batch, head) slices is compared."""
     q, k, v, do = workload_inputs(w)
