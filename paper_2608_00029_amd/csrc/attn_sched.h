@@ -35,14 +35,21 @@ constexpr int ring_in_flight_full(int split, int ahead, int need) { return (ahea
 // GPU in rounds of `band` (one per compute unit): group b shares its compute
 // unit with groups b +- band, b +- 2 band, ...  Every other round walks the
 // ranks backwards, so that a compute unit that receives one of the heaviest
-// items in one round receives one of the lightest of the next.  band <= 0
-// keeps the plain heaviest-first order.  A permutation of [0, n).
+// items in one round receives one of the lightest of the next.  The walk is
+// backwards in steps of kXcdGroup, keeping each rank's position within its
+// group of kXcdGroup: work groups are dealt to the GPU's kXcdGroup chiplets
+// (each with its own L2) round-robin by index, and a rank keeps the chiplet of
+// the same-numbered group, so the tiles of one head, which share K/V or
+// Q/dO, stay in one L2.  band <= 0 keeps the plain heaviest-first order.  A
+// permutation of [0, n).
+constexpr int kXcdGroup = 8;
 constexpr int banded_rank(int bid, int n, int band) {
   if (band <= 0) return bid;
   const int r = bid / band, p = bid % band;
   if ((r & 1) == 0) return bid;
   const int size = n - r * band < band ? n - r * band : band;
-  return r * band + size - 1 - p;
+  if (size % kXcdGroup != 0 || band % kXcdGroup != 0) return r * band + size - 1 - p;
+  return r * band + (size / kXcdGroup - 1 - p / kXcdGroup) * kXcdGroup + p % kXcdGroup;
 }
 
 }  // namespace cattn
