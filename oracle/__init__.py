@@ -1,4 +1,4 @@
-"""CPU float64 reference for fused causal attention -- test infrastructure only.
+"""CPU float64 references for fused causal attention and the fused loss head -- test infrastructure only.
 
 Only the tests, the smoke check and the CPU-baseline leg of the benchmark use
 this package; the HIP library and its binding never import it.
