@@ -171,6 +171,50 @@ def time_workload(w, bd, steps: int, warmup: int, layout: str = "bhsd"):
             "pct_peak": round(100.0 * (fwd_f + bwd_f) / (out["step"] * 1e-3) / 1e12 / PEAK_TFLOPS[w.dtype], 2)}
 
 
+def time_lmhead(wl, bd, steps: int, warmup: int):
+    """The fused loss head (projection with per-tile softmax statistics, merge,
+    mean) at one shape, inputs resident in HBM: mean ms per call over `steps`
+    calls, timed with HIP events on the stream the kernels run on.  Algorithmic
+    work: 2*M*N*K FLOPs; bytes: X and W read once, float32 logits written once,
+    the partials written and read once, LSE and the row losses written."""
+    import ctypes
+    import torch
+    from paper_2608_00029_amd.workloads import make_lmhead_inputs
+    dev = torch.device("cuda:0")
+    x, w, y = (t.to(dev) for t in make_lmhead_inputs(wl.M, wl.N, wl.K, wl.w_sigma, wl.seed))
+    z = torch.empty((wl.M, wl.N), dtype=torch.float32, device=dev)
+    lse, rl = (torch.empty((wl.M,), dtype=torch.float32, device=dev) for _ in range(2))
+    loss = torch.empty((1,), dtype=torch.float32, device=dev)
+    ws = torch.empty((bd.lmhead_workspace_bytes(wl.M, wl.N, wl.K) // 4,), dtype=torch.float32, device=dev)
+    L = bd.lib()
+    stream = torch.cuda.current_stream(dev)
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    args = [t.data_ptr() for t in (x, w, y, z, lse, rl, loss, ws)]
+
+    def call():
+        st = L.cattn_lmhead_fwd(*args, wl.M, wl.N, wl.K, sp)
+        if st != 0:
+            raise RuntimeError(f"{wl.name}: {bd.last_error_string()}")
+
+    for _ in range(warmup):
+        call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    flops = 2.0 * wl.M * wl.N * wl.K
+    nbytes = 2 * (wl.M + wl.N) * wl.K + 4 * wl.M * wl.N + 2 * 8 * wl.M * (wl.N // 64) + 4 * 3 * wl.M
+    return {"M": wl.M, "N": wl.N, "K": wl.K, "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+            "pct_mfma_peak": round(100.0 * flops / (ms * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"], 2),
+            "hbm_gbs_algorithmic": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "floor_us": {"mfma": round(flops / (PEAK_TFLOPS["bf16"] * 1e12) * 1e6, 1),
+                         "hbm": round(nbytes / (HBM_PEAK_GBS * 1e9) * 1e6, 1)}}
+
+
 def copy_probe(mib: int) -> int:
     """A plain copy of known size: it reads and writes exactly mib MiB per launch."""
     import torch
@@ -309,6 +353,8 @@ def main() -> int:
         line["configs"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in WORKLOADS}
         line["configs"][w.name + "_bshd"] = time_workload(w, bd, steps=20, warmup=5, layout="bshd")
         line["sweep"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in SWEEP}
+        from paper_2608_00029_amd.workloads import LMHEAD_WORKLOADS
+        line["lmhead"] = {c.name: time_lmhead(c, bd, steps=20, warmup=3) for c in LMHEAD_WORKLOADS}
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, cpu_inputs, args.cpu_seconds)
     print(json.dumps(line), flush=True)

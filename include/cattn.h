@@ -170,6 +170,47 @@ cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v,
                                  int B, int H, int S, int D,
                                  float scale, int causal, int dtype, void* stream);
 
+/*
+ * Fused language-model loss head, forward (section 4.1, case study "Fusing a
+ * Reduction into a Contraction Epilogue"; the fused loss-head evaluation).
+ * For hidden states X, the head's weight W (no bias) and target ids y:
+ *
+ *     Z    = X W^T                          logits
+ *     LSE  = log sum_j exp(Z[i, j])         per row, natural log
+ *     l_i  = LSE_i - Z[i, y_i]              softmax cross entropy of row i
+ *     loss = (1/M) sum_i l_i
+ *
+ * The projection keeps each row's maximum and sum of exponentials over every
+ * 64 consecutive vocabulary entries in its epilogue (partials [M, N/64]); a
+ * merge then combines the partials with the rescale-by-maximum-difference rule
+ * into LSE and l, and a fixed-order reduction forms the mean.  Deterministic.
+ *
+ *   x        : in,  [M, K] bfloat16, row-major
+ *   w        : in,  [N, K] bfloat16, row-major (one row per vocabulary entry)
+ *   targets  : in,  [M] int32 ids in [0, N), or NULL (then row_loss and loss
+ *              are not written and may be NULL); an id outside [0, N) makes
+ *              that row's loss (and the mean) NaN
+ *   logits   : out, [M, N] float (float32 accumulation of bf16 products)
+ *   lse      : out, [M] float
+ *   row_loss : out, [M] float (with targets)
+ *   loss     : out, [1] float, the mean of row_loss (with targets; may be NULL)
+ *   workspace: scratch of at least cattn_lmhead_workspace_bytes(M, N, K) bytes,
+ *              4-byte aligned; on return it holds the partials, float
+ *              [M][N/64][2] (maximum, sum of exp(z - maximum)).
+ * Supported: M a multiple of 128, N a multiple of 128, K a multiple of 64
+ * (GPT-2's head: M = 8192 tokens, K = 768, N = 50304, the vocabulary padded
+ * to a multiple of 128); otherwise CATTN_ERR_UNSUPPORTED.  M, N or K equal
+ * to 0 is an empty problem (CATTN_OK, nothing touched).  Outputs must not
+ * overlap inputs, each other or the workspace (CATTN_ERR_INVALID_ARG).
+ */
+cattn_status cattn_lmhead_fwd(const void* x, const void* w, const int* targets,
+                              float* logits, float* lse, float* row_loss, float* loss,
+                              float* workspace, int M, int N, int K, void* stream);
+
+/* Bytes of workspace cattn_lmhead_fwd needs: M * (N / 64) * 2 * sizeof(float)
+ * (0 for an empty or unsupported shape). */
+size_t cattn_lmhead_workspace_bytes(int M, int N, int K);
+
 /* Bytes of workspace cattn_attn_bwd needs: 2 * B * H * Sp * sizeof(float),
  * Sp = S rounded up to a multiple of 32 (0 for an empty or invalid shape). */
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);

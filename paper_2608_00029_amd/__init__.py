@@ -5,5 +5,6 @@ include/cattn.h); this package only marshals torch tensors into that ABI.
 """
 from .binding import (  # noqa: F401
     CattnError, attn_bwd, attn_bwd_dkdv, attn_bwd_dq, attn_fwd, last_error_string, library_path, status_string, workspace_bytes,
+    lmhead_fwd, lmhead_workspace_bytes,
     CATTN_BF16, CATTN_F32, CATTN_OK, CATTN_ERR_HIP, CATTN_ERR_INVALID_ARG, CATTN_ERR_UNSUPPORTED, CATTN_BHSD, CATTN_BSHD,
 )

@@ -25,7 +25,7 @@ CATTN_BHSD, CATTN_BSHD = 0, 1
 _LAYOUTS = {"bhsd": CATTN_BHSD, "bshd": CATTN_BSHD}
 
 EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_attn_fwd_ex", "cattn_attn_bwd_ex", "cattn_attn_bwd_dq",
-            "cattn_attn_bwd_dkdv",
+            "cattn_attn_bwd_dkdv", "cattn_lmhead_fwd", "cattn_lmhead_workspace_bytes",
             "cattn_bwd_workspace_bytes", "cattn_status_string", "cattn_last_error_string")
 
 
@@ -60,6 +60,10 @@ def lib() -> ctypes.CDLL:
         L.cattn_attn_bwd_dq.restype = i
         L.cattn_attn_bwd_dkdv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
         L.cattn_attn_bwd_dkdv.restype = i
+        L.cattn_lmhead_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, vp]
+        L.cattn_lmhead_fwd.restype = i
+        L.cattn_lmhead_workspace_bytes.argtypes = [i, i, i]
+        L.cattn_lmhead_workspace_bytes.restype = ctypes.c_size_t
         L.cattn_bwd_workspace_bytes.argtypes = [i, i, i, i]
         L.cattn_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.cattn_status_string.argtypes = [i]
@@ -241,3 +245,40 @@ def raw_bwd(q_ptr, k_ptr, v_ptr, o_ptr, do_ptr, lse_ptr, dq_ptr, dk_ptr, dv_ptr,
     return lib().cattn_attn_bwd(vp(q_ptr), vp(k_ptr), vp(v_ptr), vp(o_ptr), vp(do_ptr), vp(lse_ptr),
                                 vp(dq_ptr), vp(dk_ptr), vp(dv_ptr), vp(ws_ptr), B, H, S, D, float(scale),
                                 int(causal), int(dtype), vp(stream))
+
+
+def lmhead_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(lib().cattn_lmhead_workspace_bytes(M, N, K))
+
+
+def lmhead_fwd(x, w, targets=None, workspace=None):
+    """Fused loss head: (logits [M, N] float32, lse [M], row_loss [M] or None, loss [1] or None).
+
+    x: [M, K] bfloat16 hidden states; w: [N, K] bfloat16 head weight (one row per
+    vocabulary entry); targets: [M] int32 ids or None.  Enqueued on torch's
+    current stream; the partial statistics land in `workspace` (float32).
+    """
+    if x.dim() != 2 or w.dim() != 2:
+        raise ValueError("x must be [M, K] and w [N, K]")
+    M, K = x.shape
+    N = w.shape[0]
+    if x.device.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    _check("x", x, (M, K), torch.bfloat16, x.device)
+    _check("w", w, (N, K), torch.bfloat16, x.device)
+    if targets is not None:
+        _check("targets", targets, (M,), torch.int32, x.device)
+    logits = torch.empty((M, N), dtype=torch.float32, device=x.device)
+    lse = torch.empty((M,), dtype=torch.float32, device=x.device)
+    row_loss = torch.empty((M,), dtype=torch.float32, device=x.device) if targets is not None else None
+    loss = torch.empty((1,), dtype=torch.float32, device=x.device) if targets is not None else None
+    nws = lmhead_workspace_bytes(M, N, K) // 4
+    if workspace is None:
+        workspace = torch.empty((max(nws, 1),), dtype=torch.float32, device=x.device)
+    _check_workspace(workspace, nws, x.device)
+    st = lib().cattn_lmhead_fwd(_ptr(x), _ptr(w), _ptr(targets), _ptr(logits), _ptr(lse), _ptr(row_loss),
+                                _ptr(loss), _ptr(workspace), M, N, K, _stream(x.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_lmhead_fwd", last_error_string())
+    return logits, lse, row_loss, loss
+

@@ -27,12 +27,9 @@
 
 #include "attn_device.h"
 #include "attn_launch.h"
+#include "bf16_stream.h"
 
 namespace cattn {
-
-typedef __bf16 bf16;
-typedef Mma<bf16> MB;
-template <int N> using IC = std::integral_constant<int, N>;
 
 // Ring depths (buffers of 32-row tiles).  The forward at D = 64 runs two key
 // parts per workgroup, each with its own ring.
@@ -60,159 +57,6 @@ template <int N> using IC = std::integral_constant<int, N>;
 #ifndef CATTN_DKDV_NB64S  // dQ and dK/dV at D = 64 with the loop range split in two (two rings)
 #define CATTN_DKDV_NB64S 4
 #endif
-
-// f(IC<0>{}), f(IC<1>{}), ..., f(IC<N-1>{}), in order.
-template <typename F, int... I>
-__device__ __forceinline__ void unroll_each(F& f, std::integer_sequence<int, I...>) {
-  (f(IC<I>{}), ...);
-}
-template <int N, typename F> __device__ __forceinline__ void unroll(F&& f) {
-  unroll_each(f, std::make_integer_sequence<int, N>{});
-}
-
-template <int D> struct TileGeom {
-  static constexpr int TILE = 32 * D * 2;                 // bytes of one tensor's 32-row tile
-  static constexpr int CPR = D * 2 / 16;                  // 16-byte chunks per row
-  static constexpr int DMA_PER_TENSOR = TILE / 16 / 256;  // copy instructions per thread
-};
-
-// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 30] (expcnt and lgkmcnt left
-// at their maxima), through the builtin so that the compiler's own wait
-// bookkeeping sees it.
-__device__ __forceinline__ void wait_vm(int n) {
-#define CATTN_VMW(k) \
-  case k:            \
-    __builtin_amdgcn_s_waitcnt(0x0F70 | ((k) & 15) | (((k) >> 4) << 14)); \
-    break;
-  switch (n) {
-    CATTN_VMW(0) CATTN_VMW(1) CATTN_VMW(2) CATTN_VMW(3) CATTN_VMW(4) CATTN_VMW(5) CATTN_VMW(6) CATTN_VMW(7)
-    CATTN_VMW(8) CATTN_VMW(9) CATTN_VMW(10) CATTN_VMW(11) CATTN_VMW(12) CATTN_VMW(13) CATTN_VMW(14)
-    CATTN_VMW(15) CATTN_VMW(16) CATTN_VMW(17) CATTN_VMW(18) CATTN_VMW(19) CATTN_VMW(20) CATTN_VMW(21)
-    CATTN_VMW(22) CATTN_VMW(23) CATTN_VMW(24) CATTN_VMW(25) CATTN_VMW(26) CATTN_VMW(27) CATTN_VMW(28)
-    CATTN_VMW(29) CATTN_VMW(30)
-    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-  }
-#undef CATTN_VMW
-}
-
-// Publish a tile: wait until at most n of this wave's copies are in flight
-// (the newest ones, which target later tiles) and all of its LDS reads have
-// returned, then meet the other waves at the barrier.  A plain s_barrier: the
-// release fence of __syncthreads() would wait for every copy in flight and
-// undo the prefetch distance.  The asm memory clobber keeps the compiler from
-// moving LDS accesses across the barrier.
-__device__ __forceinline__ void tile_barrier(int n) {
-#define CATTN_TBW(k) \
-  case k:            \
-    __builtin_amdgcn_s_waitcnt(0x0070 | ((k) & 15) | (((k) >> 4) << 14)); \
-    break;
-  switch (n) {
-    CATTN_TBW(0) CATTN_TBW(1) CATTN_TBW(2) CATTN_TBW(3) CATTN_TBW(4) CATTN_TBW(5) CATTN_TBW(6) CATTN_TBW(7)
-    CATTN_TBW(8) CATTN_TBW(9) CATTN_TBW(10) CATTN_TBW(11) CATTN_TBW(12) CATTN_TBW(13) CATTN_TBW(14)
-    CATTN_TBW(15) CATTN_TBW(16) CATTN_TBW(17) CATTN_TBW(18) CATTN_TBW(19) CATTN_TBW(20) CATTN_TBW(21)
-    CATTN_TBW(22) CATTN_TBW(23) CATTN_TBW(24) CATTN_TBW(25) CATTN_TBW(26) CATTN_TBW(27) CATTN_TBW(28)
-    CATTN_TBW(29) CATTN_TBW(30)
-    default: __builtin_amdgcn_s_waitcnt(0x0070); break;
-  }
-#undef CATTN_TBW
-  asm volatile("s_barrier" ::: "memory");
-}
-
-// tile_barrier(N) for a compile-time N: a single s_waitcnt.
-template <int N> __device__ __forceinline__ void tile_barrier_c() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
-  asm volatile("s_barrier" ::: "memory");
-}
-
-// Byte address of an LDS location (the value M0 takes).
-__device__ __forceinline__ unsigned lds_addr(const char* p) {
-  return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
-}
-
-// One 16-byte HBM -> LDS copy per active lane: lane i copies the 16 bytes at
-// sbase + voff (sbase wave-uniform, in scalar registers) to LDS byte address
-// lds + 16 * i.  Issued as inline assembly so that the compiler does not treat
-// every later LDS read as aliasing the copy in flight (it would then wait for
-// the copy before each read); completion is awaited explicitly (wait_vm /
-// tile_barrier) before the barrier that publishes a tile.
-// M0 is a reserved register to the compiler, which warns about the clobber;
-// the clobber is what keeps it from assuming M0 survives the statement.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void* sbase, unsigned voff, unsigned lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// HBM -> LDS copy of 32-row tiles of an [S][D] bf16 matrix whose rows are rs elements apart.  The
-// chunk a lane deposits at physical position p of the tile is logical chunk
-// p ^ swz(row), so the LDS image has the swizzled layout Tile<> reads.  The
-// per-lane source offsets inside a tile are fixed for the kernel; only the
-// ragged last tile (rows >= nrows are read from row nrows - 1) recomputes them.
-template <int D> struct TileCopy {
-  typedef TileGeom<D> G;
-  unsigned voff[G::DMA_PER_TENSOR];
-  int w, lane, rs;
-  __device__ __forceinline__ void init(int w_, int lane_, int rs_) {
-    w = w_;
-    lane = lane_;
-    rs = rs_;
-#pragma unroll
-    for (int i = 0; i < G::DMA_PER_TENSOR; ++i) {
-      const int p = i * 256 + w * 64 + lane;
-      const int row = p / G::CPR;
-      voff[i] = (unsigned)(row * rs * 2 + (((p % G::CPR) ^ swz(row)) << 4));
-    }
-  }
-  // a tile known to lie inside the sequence (row0 + 32 <= nrows)
-  __device__ __forceinline__ void copy_full(const bf16* g, int row0, char* lds) const {
-    const bf16* src = g + (int64_t)row0 * rs;
-    const unsigned dst = lds_addr(lds) + w * 64 * 16;
-#pragma unroll
-    for (int i = 0; i < G::DMA_PER_TENSOR; ++i) dma16(src, voff[i], dst + i * 256 * 16);
-  }
-  __device__ __forceinline__ void copy(const bf16* g, int row0, int nrows, char* lds) const {
-    const bf16* src = g + (int64_t)row0 * rs;
-    const unsigned dst = lds_addr(lds) + w * 64 * 16;
-    if (row0 + 32 <= nrows) {
-#pragma unroll
-      for (int i = 0; i < G::DMA_PER_TENSOR; ++i) dma16(src, voff[i], dst + i * 256 * 16);
-    } else {
-#pragma unroll
-      for (int i = 0; i < G::DMA_PER_TENSOR; ++i) {
-        const int p = i * 256 + w * 64 + lane;
-        const int row = p / G::CPR, lc = (p % G::CPR) ^ swz(row);
-        const int src_row = min(row, nrows - 1 - row0);
-        dma16(src, (unsigned)(src_row * rs * 2 + lc * 16), dst + i * 256 * 16);
-      }
-    }
-  }
-};
-
-// Row-major A-operand fragments of the 32 rows of a tile.
-template <int D>
-__device__ __forceinline__ void read_rows(const char* lds, int r, int h, MB::frag (&f)[D / 16]) {
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) f[ks] = read_row_frag<bf16, D>(lds, r, ks, h);
-}
-
-// Transposed A-operand fragments (columns 32*dt..) of the 32 rows of a tile.
-template <int D>
-__device__ __forceinline__ void read_trans(const char* lds, int lane, MB::frag (&f)[2][D / 32]) {
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) f[s][dt] = TransRead<bf16, D>::read(lds, 0, s, dt * 32, lane);
-}
-
-// Flip the sign of every element of a bf16 fragment.
-__device__ __forceinline__ MB::frag negated(MB::frag f) {
-  u32x4 u = __builtin_bit_cast(u32x4, f);
-  u ^= 0x80008000u;
-  return __builtin_bit_cast(MB::frag, u);
-}
 
 // The forward keeps a softmax offset that moves only when a block's partial
 // probability sum exceeds this bound (or is not finite).  Probabilities are

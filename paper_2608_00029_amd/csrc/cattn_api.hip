@@ -9,6 +9,7 @@
 
 #include "../../include/cattn.h"
 #include "attn_launch.h"
+#include "lmhead_launch.h"
 
 extern "C" size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);
 
@@ -171,6 +172,43 @@ cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
                                  float scale, int causal, int dtype, void* stream) {
   return bwd_common(q, k, v, nullptr, dout, lse, nullptr, dk, dv, const_cast<float*>(workspace), B, H, S, D,
                     scale, causal, dtype, CATTN_BHSD, stream, 2);
+}
+
+size_t cattn_lmhead_workspace_bytes(int M, int N, int K) {
+  if (M <= 0 || N <= 0 || K <= 0 || M % 128 || N % 128 || K % 64) return 0;
+  return (size_t)M * (size_t)(N / 64) * 2 * sizeof(float);
+}
+
+cattn_status cattn_lmhead_fwd(const void* x, const void* w, const int* targets, float* logits, float* lse,
+                              float* row_loss, float* loss, float* workspace, int M, int N, int K, void* stream) {
+  g_last_error[0] = '\0';
+  if (M < 0 || N < 0 || K < 0) return fail(CATTN_ERR_INVALID_ARG, "negative M, N or K");
+  if (M == 0 || N == 0 || K == 0) return CATTN_OK;
+  if (M % 128 || N % 128 || K % 64) return fail(CATTN_ERR_UNSUPPORTED, "M and N must be multiples of 128, K of 64");
+  if ((int64_t)M * N > (int64_t(1) << 40) || cattn::lmhead_grid_blocks(M, N) >= (int64_t(1) << 31))
+    return fail(CATTN_ERR_UNSUPPORTED, "problem too large");
+  if (!x || !w || !logits || !lse || !workspace || (targets && !row_loss))
+    return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  if (((uintptr_t)workspace & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "workspace must be 4-byte aligned");
+  Range ins[3], outs[5];
+  int ni = 0, no = 0;
+  ins[ni++] = range_of(x, (size_t)M * K * 2);
+  ins[ni++] = range_of(w, (size_t)N * K * 2);
+  if (targets) ins[ni++] = range_of(targets, (size_t)M * 4);
+  outs[no++] = range_of(logits, (size_t)M * N * 4);
+  outs[no++] = range_of(lse, (size_t)M * 4);
+  outs[no++] = range_of(workspace, cattn_lmhead_workspace_bytes(M, N, K));
+  if (targets) outs[no++] = range_of(row_loss, (size_t)M * 4);
+  if (targets && loss) outs[no++] = range_of(loss, 4);
+  for (int i = 0; i < no; ++i)
+    for (int j = 0; j < ni; ++j)
+      if (overlap(outs[i], ins[j])) return fail(CATTN_ERR_INVALID_ARG, "an output or the workspace overlaps an input");
+  for (int i = 0; i < no; ++i)
+    for (int j = i + 1; j < no; ++j)
+      if (overlap(outs[i], outs[j])) return fail(CATTN_ERR_INVALID_ARG, "outputs or workspace overlap each other");
+  cattn::LmheadArgs a{x, w, targets, logits, lse, row_loss, targets ? loss : nullptr, workspace, M, N, K};
+  (void)hipGetLastError();
+  return hip_status(cattn::launch_lmhead(a, (hipStream_t)stream));
 }
 
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D) {

@@ -101,3 +101,33 @@ def make_inputs(B: int, H: int, S: int, D: int, dtype: str = "bf16", seed: int =
 
 def workload_inputs(w: Workload):
     return make_inputs(w.B, w.H, w.S, w.D, w.dtype, w.seed, w.qk_sigma)
+
+
+@dataclass(frozen=True)
+class LmheadWorkload:
+    """Fused loss-head shape: M tokens of hidden size K against an N-entry vocabulary."""
+    name: str
+    M: int
+    N: int
+    K: int
+    w_sigma: float
+    seed: int
+
+
+# GPT-2 124M's head as the paper trains and measures it: 8 sequences of 1024
+# tokens (M = 8192), hidden size 768, vocabulary 50257 padded to 50304.
+LMHEAD_WORKLOADS = [
+    LmheadWorkload("gpt2_lmhead_M8192_N50304_K768", 8192, 50304, 768, 0.02, SEED_BASE + 20),
+]
+
+
+def make_lmhead_inputs(M: int, N: int, K: int, w_sigma: float = 0.02, seed: int = SEED_BASE):
+    """(x [M, K] bf16, w [N, K] bf16, targets [M] int32) CPU tensors: x ~ N(0, 1) (hidden states
+    after the final normalisation), w ~ N(0, w_sigma^2) (GPT-2's embedding initialisation), targets
+    uniform over the vocabulary.  Drawn in that order from one seeded CPU generator."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    x = torch.randn((M, K), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    w = (torch.randn((N, K), generator=g, dtype=torch.float32) * w_sigma).to(torch.bfloat16)
+    y = torch.randint(0, N, (M,), generator=g, dtype=torch.int64).to(torch.int32)
+    return x.contiguous(), w.contiguous(), y.contiguous()
+

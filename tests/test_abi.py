@@ -133,3 +133,34 @@ def test_empty_problem_in_either_layout_is_a_noop(lib):
     vp = __import__("ctypes").c_void_p
     for layout in (b.CATTN_BHSD, b.CATTN_BSHD):
         assert lib.cattn_attn_fwd_ex(*[vp(0)] * 5, 0, 2, 64, 64, 0.125, 1, 1, layout, vp(0)) == b.CATTN_OK
+
+
+def test_lmhead_workspace_bytes(lib):
+    assert b.lmhead_workspace_bytes(8192, 50304, 768) == 8192 * (50304 // 64) * 2 * 4
+    assert b.lmhead_workspace_bytes(128, 128, 64) == 128 * 2 * 2 * 4
+    assert b.lmhead_workspace_bytes(0, 128, 64) == 0
+    assert b.lmhead_workspace_bytes(100, 128, 64) == 0  # unsupported shape
+
+
+def test_lmhead_argument_errors(lib):
+    vp = ctypes.c_void_p
+    x, w, y, z, lse, rl, loss, ws = (vp(p) for p in P[:8])
+    M, N, K = 128, 256, 64
+
+    def call(*a, M=M, N=N, K=K):
+        return lib.cattn_lmhead_fwd(*a, M, N, K, vp(0))
+
+    assert call(x, w, y, z, lse, rl, loss, ws, M=-1) == b.CATTN_ERR_INVALID_ARG
+    assert call(x, w, y, z, lse, rl, loss, ws, M=0) == b.CATTN_OK          # empty problem: nothing touched
+    assert call(x, w, y, z, lse, rl, loss, ws, K=0) == b.CATTN_OK
+    assert call(x, w, y, z, lse, rl, loss, ws, M=100) == b.CATTN_ERR_UNSUPPORTED
+    assert call(x, w, y, z, lse, rl, loss, ws, N=200) == b.CATTN_ERR_UNSUPPORTED
+    assert call(x, w, y, z, lse, rl, loss, ws, K=96) == b.CATTN_ERR_UNSUPPORTED
+    assert call(vp(0), w, y, z, lse, rl, loss, ws) == b.CATTN_ERR_INVALID_ARG
+    assert call(x, w, y, z, lse, vp(0), loss, ws) == b.CATTN_ERR_INVALID_ARG  # targets need row_loss
+    assert call(x, w, y, z, lse, rl, loss, vp(0)) == b.CATTN_ERR_INVALID_ARG
+    assert call(x, w, y, z, lse, rl, loss, vp(P[7] + 2)) == b.CATTN_ERR_INVALID_ARG  # misaligned workspace
+    assert call(x, w, y, vp(P[0]), lse, rl, loss, ws) == b.CATTN_ERR_INVALID_ARG     # logits alias x
+    assert call(x, w, y, z, vp(P[3] + 64), rl, loss, ws) == b.CATTN_ERR_INVALID_ARG  # lse inside logits
+    assert call(x, w, y, z, lse, rl, loss, vp(P[1] + 4)) == b.CATTN_ERR_INVALID_ARG  # workspace inside w
+    assert "overlap" in b.last_error_string()
