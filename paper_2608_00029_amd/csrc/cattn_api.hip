@@ -185,7 +185,7 @@ cattn_status cattn_lmhead_fwd(const void* x, const void* w, const int* targets, 
   if (M < 0 || N < 0 || K < 0) return fail(CATTN_ERR_INVALID_ARG, "negative M, N or K");
   if (M == 0 || N == 0 || K == 0) return CATTN_OK;
   if (M % 128 || N % 128 || K % 64) return fail(CATTN_ERR_UNSUPPORTED, "M and N must be multiples of 128, K of 64");
-  if ((int64_t)M * N > (int64_t(1) << 40) || cattn::lmhead_grid_blocks(M, N) >= (int64_t(1) << 31))
+  if ((int64_t)M * N > (int64_t(1) << 40) || M > (1 << 24) || N > (1 << 23))
     return fail(CATTN_ERR_UNSUPPORTED, "problem too large");
   if (!x || !w || !logits || !lse || !workspace || (targets && !row_loss))
     return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");

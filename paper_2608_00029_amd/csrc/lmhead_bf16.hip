@@ -6,19 +6,27 @@
 // per-tile partials into LSE and the per-row cross entropy, and reduce the
 // per-row losses to their mean.
 //
-// Kernel 1 (projection + statistics).  A work group owns 128 vocabulary rows
-// x 128 tokens of Z and streams K in chunks of 64 through a ring of LDS slots
-// (W tile and X tile of a chunk, 32 KB).  Each of its four waves computes a
-// 64 x 64 block as 2 x 2 transposed 32 x 32 matrix-core blocks, Z^T = W X^T,
-// so that every lane holds one token and 16 vocabulary entries of each block:
-// the row statistics are then in-lane over 32 entries plus one swap between
-// the wave halves, exactly as the attention kernels' row softmax.  A wave's
-// partial covers its 64 vocabulary entries: partials are [M, N/64] pairs
-// (maximum, sum of exp(z - maximum)).  Logits are written as float [M, N].
+// Kernel 1 (projection + statistics).  A persistent grid of one work group
+// per compute unit; each walks its chiplet's 256 x 256 output tiles (256
+// vocabulary rows x 256 tokens of Z) and streams K in chunks of 64 through two
+// LDS slots (W and X rows of a chunk, 64 KB each): the copy of chunk c + 1 --
+// or of the next tile's first chunk -- runs while chunk c computes, so the
+// next tile's first copy also overlaps this tile's epilogue.  Each of the
+// eight waves computes a 128 x 64 block as 4 x 2 transposed 32 x 32
+// matrix-core blocks, Z^T = W X^T, so that every lane holds one token and 16
+// vocabulary entries of each block: the row statistics are then in-lane over
+// 32 entries plus one swap between the wave halves, exactly as the attention
+// kernels' row softmax.  A partial covers 64 vocabulary entries: partials are
+// [M, N/64] pairs (maximum, sum of exp(z - maximum)).  Logits are written as
+// float [M, N].  A 256 x 256 tile does 128 FLOPs per byte it brings into LDS,
+// twice what a 128 x 128 tile does, which is what keeps the chiplets' L2
+// bandwidth from capping the matrix cores.
 //
-// Work groups are dealt to the GPU's chiplets round-robin by index; a
-// chiplet's groups walk its vocabulary tiles eight at a time with the token
-// tiles inside, so the W and X tiles in flight on one chiplet fit its L2.
+// Tiles are dealt to the GPU's chiplets by vocabulary tile (modulo 8); a
+// chiplet walks its vocabulary tiles eight at a time with the token tiles
+// inside (lmhead_sched.h), so the W and X rows in flight on it fit its L2.
+// A ragged last tile (N or M not a multiple of 256; both are multiples of
+// 128) leaves the waves past the end idle and skips their copies.
 //
 // Kernel 2 (merge): one wave per token row combines the row's N/64 partials
 // with the rescale-by-maximum-difference rule (the merge is not the fold),
@@ -29,132 +37,126 @@
 #include "attn_device.h"
 #include "bf16_stream.h"
 #include "lmhead_launch.h"
+#include "lmhead_sched.h"
 
 namespace cattn {
 
-#ifndef CATTN_LMH_NB
-#define CATTN_LMH_NB 2
-#endif
-
-constexpr int kLmhTileV = 128;  // vocabulary rows per work group
-constexpr int kLmhTileM = 128;  // tokens per work group
-constexpr int kLmhKC = 64;      // K chunk per ring slot
-constexpr int kLmhPartW = 64;   // vocabulary entries per partial
-
-// Work group -> (vocabulary tile, token tile), or false for a padding group.
-__device__ __forceinline__ bool lmh_tile_of_block(int bid, int n_vt, int n_mt, int& vt, int& mt) {
-  const int x = bid % kXcdGroup, l = bid / kXcdGroup;
-  const int nv_x = (n_vt - x + kXcdGroup - 1) / kXcdGroup;  // vocabulary tiles of chiplet x: x, x + 8, ...
-  if (x >= n_vt || l >= nv_x * n_mt) return false;
-  const int vb = l / (8 * n_mt);
-  const int g = min(8, nv_x - 8 * vb);
-  const int rem = l - vb * 8 * n_mt;
-  mt = rem / g;
-  vt = x + kXcdGroup * (8 * vb + rem % g);
-  return true;
-}
-
-template <int NB>
-__global__ __launch_bounds__(256) void lmhead_logits_stats_kernel(const bf16* __restrict__ X,
+__global__ __launch_bounds__(512) void lmhead_logits_stats_kernel(const bf16* __restrict__ X,
                                                                   const bf16* __restrict__ W,
                                                                   float* __restrict__ Z, float* __restrict__ part,
-                                                                  int M, int N, int K, int n_vt, int n_mt) {
-  constexpr int TILE = 32 * kLmhKC * 2;  // one 32-row tile of a chunk: 4 KB
-  constexpr int SLOT = 8 * TILE;         // W: 4 tiles (128 rows), X: 4 tiles (128 rows)
-  constexpr int AH = NB - 1, PER_CHUNK = 8 * TileGeom<kLmhKC>::DMA_PER_TENSOR;
+                                                                  int M, int N, int K, int per_xcd) {
+  constexpr int TILE = 32 * kLmhKC * 2;  // one 32-row block of a chunk: 4 KB
+  constexpr int SLOT = 16 * TILE;        // W: 8 blocks (256 rows), X: 8 blocks (256 rows)
   constexpr int KS = kLmhKC / 16;
-  __shared__ __attribute__((aligned(16))) char smem[NB * SLOT];
+  __shared__ __attribute__((aligned(16))) char smem[2 * SLOT];
 
-  int vt, mt;
-  if (!lmh_tile_of_block(blockIdx.x, n_vt, n_mt, vt, mt)) return;  // uniform over the group
+  const int n_vt = lmh_vtiles(N), n_mt = lmh_mtiles(M);
+  const int x = blockIdx.x % kXcdGroup;
+  const int n_tiles = lmh_xcd_tiles(x, n_vt, n_mt);
+  int l = blockIdx.x / kXcdGroup;
+  if (l >= n_tiles) return;  // uniform over the group
+
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int vw = w & 1, tw = w >> 1;  // this wave: vocabulary half, token half
-  const int v0 = vt * kLmhTileV, m0 = mt * kLmhTileM;
+  const int vw = w & 1, tw = w >> 1;  // this wave: vocabulary half (128 rows), token quarter (64)
   const int n_chunks = K / kLmhKC;
+  const int n_part = N / kLmhPartW;
 
+  // Waves 0-3 copy the W rows of a chunk, waves 4-7 its X rows: eight 32-row
+  // blocks each, one 16-byte copy per lane per block.
   TileCopy<kLmhKC> tc;
-  tc.init(w, lane, K);
-  auto dma = [&](int c, auto slc) {  // chunk c into ring slot slc
-    char* b = smem + decltype(slc)::value * SLOT;
+  tc.init(w & 3, lane, K);
+  const bool copies_w = w < 4;
+  const bf16* src = copies_w ? W : X;
+  const int src_rows = copies_w ? N : M;
+  auto dma = [&](int tile, int c, int slot) {
+    const int v0 = (tile >> 16) * kLmhTileV, m0 = (tile & 0xffff) * kLmhTileM;
+    const int row0 = copies_w ? v0 : m0;
+    char* b = smem + slot * SLOT + (copies_w ? 0 : 8 * TILE);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      tc.copy_full(W + c * kLmhKC, v0 + 32 * i, b + i * TILE);
-      tc.copy_full(X + c * kLmhKC, m0 + 32 * i, b + (4 + i) * TILE);
-    }
+    for (int i = 0; i < 8; ++i)
+      if (row0 + 32 * i < src_rows) tc.copy_full(src + c * kLmhKC, row0 + 32 * i, b + i * TILE);
   };
-  unroll<AH>([&](auto I) {
-    if (decltype(I)::value < n_chunks) dma(decltype(I)::value, I);
-  });
-  wait_vm(0);
-  __syncthreads();
 
-  f32x16 acc[2][2];  // [vocabulary block][token block] of Z^T
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+  int tile = lmh_xcd_tile(x, l, n_vt, n_mt);
+  int slot = 0;
+  dma(tile, 0, 0);
+  while (true) {
+    const int v0 = (tile >> 16) * kLmhTileV, m0 = (tile & 0xffff) * kLmhTileM;
+    const int vrow = v0 + 128 * vw, tok0 = m0 + 64 * tw;
+    const bool active = vrow < N && tok0 < M;  // uniform per wave
+    const int l_next = l + per_xcd;
+    const int tile_next = l_next < n_tiles ? lmh_xcd_tile(x, l_next, n_vt, n_mt) : -1;
 
-  for (int c0 = 0; c0 < n_chunks; c0 += NB) {
-    unroll<NB>([&](auto slc) {
-      constexpr int sl = decltype(slc)::value;
-      const int c = c0 + sl;
-      if (c >= n_chunks) return;
-      if (c > 0) {  // chunk c landed (copies of later chunks may stay in flight); slot of c-1 free
-        if (c + AH - 1 < n_chunks) {
-          tile_barrier_c<(AH - 1) * PER_CHUNK>();
-        } else {
-          tile_barrier(0);
-        }
+    f32x16 acc[4][2];  // [vocabulary block][token block] of Z^T
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) acc[a][t] = f32x16{};
+
+    for (int c = 0; c < n_chunks; ++c) {
+      // chunk c landed in `slot` (the only copy in flight); every wave is done
+      // reading the other slot, which the next copy overwrites
+      tile_barrier(0);
+      if (c + 1 < n_chunks) {
+        dma(tile, c + 1, slot ^ 1);
+      } else if (tile_next >= 0) {
+        dma(tile_next, 0, slot ^ 1);
       }
-      if (c + AH < n_chunks) dma(c + AH, IC<(sl + AH) % NB>{});
-      const char* b = smem + sl * SLOT;
-      MB::frag wf[2][KS], xf[2][KS];
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
+      if (active) {
+        const char* b = smem + slot * SLOT;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          wf[blk][ks] = read_row_frag<bf16, kLmhKC>(b + (2 * vw + blk) * TILE, r, ks, h);
-          xf[blk][ks] = read_row_frag<bf16, kLmhKC>(b + (4 + 2 * tw + blk) * TILE, r, ks, h);
+          MB::frag wf[4], xf[2];
+#pragma unroll
+          for (int a = 0; a < 4; ++a) wf[a] = read_row_frag<bf16, kLmhKC>(b + (4 * vw + a) * TILE, r, ks, h);
+#pragma unroll
+          for (int t = 0; t < 2; ++t) xf[t] = read_row_frag<bf16, kLmhKC>(b + (8 + 2 * tw + t) * TILE, r, ks, h);
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) acc[a][t] = MB::run(wf[a], xf[t], acc[a][t]);
+        }
+      }
+      slot ^= 1;
+    }
+
+    // Epilogue.  acc[a][t][e]: Z[token tok0 + 32 t + r][vocab vrow + 32 a + acc_row(e, h)]
+    if (active) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int tok = tok0 + 32 * t + r;
+        float* zrow = Z + (int64_t)tok * N + vrow;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {  // two partials of 64 entries: blocks 2p, 2p + 1
+          float mx = acc[2 * p][t][0];
+#pragma unroll
+          for (int a = 2 * p; a < 2 * p + 2; ++a)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[a][t][e]);
+          mx = halves_max(mx);
+          float s = 0.f;
+#pragma unroll
+          for (int a = 2 * p; a < 2 * p + 2; ++a)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) s += exp2_hw((acc[a][t][e] - mx) * kLog2e);
+          s = halves_sum(s);
+          if (h == 0) {
+            float2* pp = (float2*)(part + ((int64_t)tok * n_part + (vrow + 64 * p) / kLmhPartW) * 2);
+            *pp = make_float2(mx, s);
+          }
         }
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int t = 0; t < 2; ++t) acc[a][t] = MB::run(wf[a][ks], xf[t][ks], acc[a][t]);
-    });
-  }
-
-  // Epilogue.  acc[a][t][e]: Z[token m0 + 64 tw + 32 t + r][vocab v0 + 64 vw + 32 a + acc_row(e, h)]
-  const int n_part = N / kLmhPartW;
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int tok = m0 + 64 * tw + 32 * t + r;
-    float mx = acc[0][t][0];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[a][t][e]);
-    mx = halves_max(mx);
-    float s = 0.f;
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) s += exp2_hw((acc[a][t][e] - mx) * kLog2e);
-    s = halves_sum(s);
-    if (h == 0) {
-      float* p = part + ((int64_t)tok * n_part + (v0 + 64 * vw) / kLmhPartW) * 2;
-      p[0] = mx;
-      p[1] = s;
+          for (int g = 0; g < 4; ++g)
+            *(f32x4*)(zrow + 32 * a + 8 * g + 4 * h) =
+                f32x4{acc[a][t][4 * g], acc[a][t][4 * g + 1], acc[a][t][4 * g + 2], acc[a][t][4 * g + 3]};
+      }
     }
-    float* zrow = Z + (int64_t)tok * N + v0 + 64 * vw;
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-        store4<float>(zrow + 32 * a + 8 * g + 4 * h, acc[a][t][4 * g], acc[a][t][4 * g + 1], acc[a][t][4 * g + 2],
-                      acc[a][t][4 * g + 3]);
+    if (tile_next < 0) break;
+    l = l_next;
+    tile = tile_next;
   }
 }
 
@@ -212,17 +214,24 @@ __global__ __launch_bounds__(256) void lmhead_mean_kernel(const float* __restric
   if (threadIdx.x == 0) loss[0] = red[0] / (float)M;
 }
 
-int64_t lmhead_grid_blocks(int M, int N) {
-  const int n_vt = N / kLmhTileV, n_mt = M / kLmhTileM;
-  const int nv_max = (n_vt + kXcdGroup - 1) / kXcdGroup;
-  return (int64_t)kXcdGroup * nv_max * n_mt;
+// Work groups per chiplet of the persistent projection grid: one per compute
+// unit (the kernel's 128 KB of LDS allows no more).
+static int lmh_per_xcd() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 32;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = imax(1, n / kXcdGroup);
+  }
+  return cached[dev];
 }
 
 hipError_t launch_lmhead(const LmheadArgs& a, hipStream_t st) {
-  const int n_vt = a.N / kLmhTileV, n_mt = a.M / kLmhTileM;
-  hipLaunchKernelGGL((lmhead_logits_stats_kernel<CATTN_LMH_NB>), dim3((unsigned)lmhead_grid_blocks(a.M, a.N)),
-                     dim3(256), 0, st, (const bf16*)a.x, (const bf16*)a.w, a.logits, a.part, a.M, a.N, a.K, n_vt,
-                     n_mt);
+  const int per_xcd = lmh_per_xcd();
+  hipLaunchKernelGGL(lmhead_logits_stats_kernel, dim3((unsigned)lmh_grid(per_xcd)), dim3(512), 0, st,
+                     (const bf16*)a.x, (const bf16*)a.w, a.logits, a.part, a.M, a.N, a.K, per_xcd);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(lmhead_merge_kernel, dim3((unsigned)((a.M + 3) / 4)), dim3(256), 0, st, (const float*)a.part,

@@ -21,6 +21,5 @@ struct LmheadArgs {
 };
 
 hipError_t launch_lmhead(const LmheadArgs& a, hipStream_t st);
-int64_t lmhead_grid_blocks(int M, int N);
 
 }  // namespace cattn

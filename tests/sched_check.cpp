@@ -5,6 +5,8 @@
 #include <initializer_list>
 
 #include "attn_sched.h"
+#include "lmhead_sched.h"
+#include <vector>
 
 using namespace cattn;
 
@@ -58,6 +60,30 @@ int main() {
   for (int S = 1; S <= 5000; ++S) {
     const int p = ws_rows(S);
     if (p % 32 != 0 || p < S || p >= S + 32) ++bad;
+  }
+  // loss-head persistent grid: every (vocabulary tile, token tile) is taken by
+  // exactly one work group, on the chiplet of its vocabulary tile, in bounds
+  for (int N : {128, 256, 384, 1152, 2304, 50304, 65536 + 128}) {
+    for (int M : {128, 256, 384, 8192}) {
+      const int n_vt = lmh_vtiles(N), n_mt = lmh_mtiles(M);
+      for (int per_xcd : {1, 3, 32}) {
+        std::vector<int> seen((size_t)n_vt * n_mt, 0);
+        for (int b = 0; b < lmh_grid(per_xcd); ++b) {
+          const int x = b % kXcdGroup;
+          for (int l = b / kXcdGroup; l < lmh_xcd_tiles(x, n_vt, n_mt); l += per_xcd) {
+            ++checks;
+            const int t = lmh_xcd_tile(x, l, n_vt, n_mt), vt = t >> 16, mt = t & 0xffff;
+            if (vt < 0 || vt >= n_vt || mt < 0 || mt >= n_mt || vt % kXcdGroup != x) {
+              ++bad;
+              continue;
+            }
+            ++seen[(size_t)vt * n_mt + mt];
+          }
+        }
+        for (int c : seen)
+          if (c != 1) ++bad;
+      }
+    }
   }
   std::printf("checks=%ld bad=%ld\n", checks, bad);
   return bad != 0 || checks == 0;

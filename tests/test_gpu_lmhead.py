@@ -20,10 +20,12 @@ derived from the arithmetic):
     GPU's own logits over the tile's 64 columns; each tile sum matches the
     float64 sum of exp(z - maximum) over those logits within 1e-5 relative.
 
-Small cases compare every element; they span several 128 x 128 output tiles,
-vocabulary-tile counts that leave some chiplets without work and some with an
-extra tile, and logit scales where the per-tile maxima differ widely (so the
-merge's rescale matters).  The GPT-2 head (M 8192, N 50304, K 768) runs at
+Small cases compare every element; they span several 256 x 256 output tiles,
+ragged last tiles in either direction (half-width tiles whose idle waves skip
+their copies), vocabulary-tile counts that leave some chiplets without work
+and some with an extra tile, work groups of the persistent grid that walk
+several tiles, and logit scales where the per-tile maxima differ widely (so
+the merge's rescale matters).  The GPT-2 head (M 8192, N 50304, K 768) runs at
 full size in the configuration the benchmark times and is compared on sampled
 rows, which the oracle computes exactly.
 """
@@ -105,6 +107,7 @@ SMALL = [
     (384, 1152, 128, 0.5, True),     # nine vocabulary tiles: chiplet 0 gets two
     (256, 2304, 320, 3.0, False),    # wide logits (sigma ~ 50): the merge rescale dominates; no targets
     (512, 1280, 768, 0.02, True),    # GPT-2's hidden size
+    (4096, 8320, 128, 0.3, True),    # 33 x 16 tiles: every work group walks two or three tiles
 ]
 
 
