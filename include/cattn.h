@@ -211,6 +211,63 @@ cattn_status cattn_lmhead_fwd(const void* x, const void* w, const int* targets,
  * (0 for an empty or unsupported shape). */
 size_t cattn_lmhead_workspace_bytes(int M, int N, int K);
 
+/*
+ * Memory-bound operators of the GPT-2 step around attention (section 6,
+ * "Memory-Bound Operators": LayerNorm, GELU and fused softmax cross entropy,
+ * forward and backward, on float32 tensors; GELU and cross entropy with their
+ * backward ops are the ops of the section 3 language-model-head IR example).
+ * Every tensor is a contiguous float32 (targets: int32) device array whose
+ * address is a multiple of 16 bytes (CATTN_ERR_INVALID_ARG otherwise);
+ * outputs must not overlap inputs or each other.  Asynchronous on `stream`,
+ * deterministic (fixed-order reductions).  A size of 0 is an empty problem.
+ *
+ * LayerNorm over the last axis of x [rows, C] (biased variance, eps inside the
+ * square root):
+ *     mean_r = (1/C) sum_c x[r,c],  rstd_r = 1 / sqrt((1/C) sum_c (x[r,c] - mean_r)^2 + eps)
+ *     y = (x - mean_r) * rstd_r * gamma + beta
+ *   x, y: [rows, C]; gamma, beta: [C]; mean, rstd: out, [rows].
+ *   Supported: C a multiple of 4 and at most 4096 (CATTN_ERR_UNSUPPORTED
+ *   otherwise); eps finite and >= 0.
+ */
+cattn_status cattn_layernorm_fwd(const float* x, const float* gamma, const float* beta,
+                                 float* y, float* mean, float* rstd,
+                                 int rows, int C, float eps, void* stream);
+
+/* LayerNorm backward for upstream dy [rows, C], with the forward's mean and
+ * rstd, xhat = (x - mean) * rstd and g = dy * gamma:
+ *     dx = rstd * (g - mean_c(g) - xhat * mean_c(g * xhat))     [rows, C]
+ *     dgamma = sum_r dy * xhat,  dbeta = sum_r dy               [C]
+ * workspace: at least cattn_layernorm_bwd_workspace_bytes(rows, C) bytes,
+ * 16-byte aligned (per-group partial sums of dgamma and dbeta). */
+cattn_status cattn_layernorm_bwd(const float* x, const float* gamma, const float* mean,
+                                 const float* rstd, const float* dy, float* dx,
+                                 float* dgamma, float* dbeta, float* workspace,
+                                 int rows, int C, void* stream);
+size_t cattn_layernorm_bwd_workspace_bytes(int rows, int C);
+
+/* GELU, the tanh form (GPT-2's activation), elementwise over n floats:
+ *     y = 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))
+ * and its backward dx = dy * dy/dx(x).  Any n >= 0. */
+cattn_status cattn_gelu_fwd(const float* x, float* y, long long n, void* stream);
+cattn_status cattn_gelu_bwd(const float* x, const float* dy, float* dx, long long n, void* stream);
+
+/* Softmax cross entropy of logits z [rows, V] against targets [rows] (int32):
+ *     lse_r = log sum_j exp(z[r,j]),  row_loss_r = lse_r - z[r, t_r],
+ *     loss = (1/rows) sum_r row_loss_r
+ * One read of the logits.  targets may be NULL (only lse is written; row_loss
+ * and loss may then be NULL); loss may be NULL.  A target outside [0, V)
+ * makes that row's loss (and the mean) NaN.  Supported: V a multiple of 4. */
+cattn_status cattn_sce_fwd(const float* logits, const int* targets, float* lse,
+                           float* row_loss, float* loss, int rows, int V, void* stream);
+
+/* Softmax cross-entropy backward, the softmax recomputed from the logits and
+ * the forward's lse (no softmax tensor is stored):
+ *     dlogits[r, j] = scale * (exp(z[r,j] - lse_r) - [j == t_r])
+ * (scale = dloss / rows for the mean loss).  A row whose target is outside
+ * [0, V) gets NaN everywhere.  Supported: V a multiple of 4; scale finite. */
+cattn_status cattn_sce_bwd(const float* logits, const int* targets, const float* lse,
+                           float scale, float* dlogits, int rows, int V, void* stream);
+
 /* Bytes of workspace cattn_attn_bwd needs: 2 * B * H * Sp * sizeof(float),
  * Sp = S rounded up to a multiple of 32 (0 for an empty or invalid shape). */
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);

@@ -26,7 +26,9 @@ _LAYOUTS = {"bhsd": CATTN_BHSD, "bshd": CATTN_BSHD}
 
 EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_attn_fwd_ex", "cattn_attn_bwd_ex", "cattn_attn_bwd_dq",
             "cattn_attn_bwd_dkdv", "cattn_lmhead_fwd", "cattn_lmhead_workspace_bytes",
-            "cattn_bwd_workspace_bytes", "cattn_status_string", "cattn_last_error_string")
+            "cattn_bwd_workspace_bytes", "cattn_status_string", "cattn_last_error_string",
+            "cattn_layernorm_fwd", "cattn_layernorm_bwd", "cattn_layernorm_bwd_workspace_bytes", "cattn_gelu_fwd",
+            "cattn_gelu_bwd", "cattn_sce_fwd", "cattn_sce_bwd")
 
 
 class CattnError(RuntimeError):
@@ -66,6 +68,21 @@ def lib() -> ctypes.CDLL:
         L.cattn_lmhead_workspace_bytes.restype = ctypes.c_size_t
         L.cattn_bwd_workspace_bytes.argtypes = [i, i, i, i]
         L.cattn_bwd_workspace_bytes.restype = ctypes.c_size_t
+        ll = ctypes.c_longlong
+        L.cattn_layernorm_fwd.argtypes = [vp] * 6 + [i, i, f, vp]
+        L.cattn_layernorm_fwd.restype = i
+        L.cattn_layernorm_bwd.argtypes = [vp] * 9 + [i, i, vp]
+        L.cattn_layernorm_bwd.restype = i
+        L.cattn_layernorm_bwd_workspace_bytes.argtypes = [i, i]
+        L.cattn_layernorm_bwd_workspace_bytes.restype = ctypes.c_size_t
+        L.cattn_gelu_fwd.argtypes = [vp, vp, ll, vp]
+        L.cattn_gelu_fwd.restype = i
+        L.cattn_gelu_bwd.argtypes = [vp, vp, vp, ll, vp]
+        L.cattn_gelu_bwd.restype = i
+        L.cattn_sce_fwd.argtypes = [vp] * 5 + [i, i, vp]
+        L.cattn_sce_fwd.restype = i
+        L.cattn_sce_bwd.argtypes = [vp, vp, vp, f, vp, i, i, vp]
+        L.cattn_sce_bwd.restype = i
         L.cattn_status_string.argtypes = [i]
         L.cattn_status_string.restype = ctypes.c_char_p
         L.cattn_last_error_string.argtypes = []
@@ -282,3 +299,129 @@ def lmhead_fwd(x, w, targets=None, workspace=None):
         raise CattnError(st, "cattn_lmhead_fwd", last_error_string())
     return logits, lse, row_loss, loss
 
+
+
+# ---------------------------------------------------------------------------
+# Memory-bound operators (float32): LayerNorm, GELU, softmax cross entropy
+# ---------------------------------------------------------------------------
+def _f32_on_device(name, t, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on a HIP device")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32, not {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _rows_cols(x):
+    if x.dim() < 1:
+        raise ValueError("x needs at least one dimension")
+    C = x.shape[-1]
+    return (x.numel() // C if C else 0), C
+
+
+def layernorm_fwd(x, gamma, beta, eps: float = 1e-5):
+    """(y, mean, rstd): LayerNorm over the last axis of float32 x; mean / rstd are [rows]."""
+    _f32_on_device("x", x)
+    R, C = _rows_cols(x)
+    _f32_on_device("gamma", gamma, (C,))
+    _f32_on_device("beta", beta, (C,))
+    y = torch.empty_like(x)
+    mean = torch.empty((R,), dtype=torch.float32, device=x.device)
+    rstd = torch.empty((R,), dtype=torch.float32, device=x.device)
+    st = lib().cattn_layernorm_fwd(_ptr(x), _ptr(gamma), _ptr(beta), _ptr(y), _ptr(mean), _ptr(rstd), R, C,
+                                   float(eps), _stream(x.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_layernorm_fwd", last_error_string())
+    return y, mean, rstd
+
+
+def layernorm_bwd_workspace_bytes(rows: int, C: int) -> int:
+    return int(lib().cattn_layernorm_bwd_workspace_bytes(rows, C))
+
+
+def layernorm_bwd(x, gamma, mean, rstd, dy, workspace=None):
+    """(dx, dgamma, dbeta) of LayerNorm for upstream dy, given the forward's mean and rstd."""
+    _f32_on_device("x", x)
+    R, C = _rows_cols(x)
+    _f32_on_device("gamma", gamma, (C,))
+    _f32_on_device("mean", mean, (R,))
+    _f32_on_device("rstd", rstd, (R,))
+    _f32_on_device("dy", dy, tuple(x.shape))
+    dx = torch.empty_like(x)
+    dgamma = torch.empty((C,), dtype=torch.float32, device=x.device)
+    dbeta = torch.empty((C,), dtype=torch.float32, device=x.device)
+    nws = layernorm_bwd_workspace_bytes(R, C) // 4
+    if workspace is None:
+        workspace = torch.empty((max(nws, 4),), dtype=torch.float32, device=x.device)
+    _check_workspace(workspace, nws, x.device)
+    st = lib().cattn_layernorm_bwd(_ptr(x), _ptr(gamma), _ptr(mean), _ptr(rstd), _ptr(dy), _ptr(dx), _ptr(dgamma),
+                                   _ptr(dbeta), _ptr(workspace), R, C, _stream(x.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_layernorm_bwd", last_error_string())
+    return dx, dgamma, dbeta
+
+
+def gelu_fwd(x):
+    """y = GELU(x), tanh form, elementwise over a float32 tensor."""
+    _f32_on_device("x", x)
+    y = torch.empty_like(x)
+    st = lib().cattn_gelu_fwd(_ptr(x), _ptr(y), x.numel(), _stream(x.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_gelu_fwd", last_error_string())
+    return y
+
+
+def gelu_bwd(x, dy):
+    """dx = dy * GELU'(x)."""
+    _f32_on_device("x", x)
+    _f32_on_device("dy", dy, tuple(x.shape))
+    dx = torch.empty_like(x)
+    st = lib().cattn_gelu_bwd(_ptr(x), _ptr(dy), _ptr(dx), x.numel(), _stream(x.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_gelu_bwd", last_error_string())
+    return dx
+
+
+def _targets(targets, R, device):
+    if targets is None:
+        return None
+    if not isinstance(targets, torch.Tensor) or targets.dtype != torch.int32 or targets.device != device \
+            or tuple(targets.shape) != (R,) or not targets.is_contiguous():
+        raise ValueError(f"targets must be a contiguous int32 tensor of shape ({R},) on {device}")
+    return targets
+
+
+def sce_fwd(logits, targets=None):
+    """(lse [rows], row_loss [rows] or None, loss [1] or None) of softmax cross entropy over the last axis."""
+    _f32_on_device("logits", logits)
+    R, V = _rows_cols(logits)
+    targets = _targets(targets, R, logits.device)
+    lse = torch.empty((R,), dtype=torch.float32, device=logits.device)
+    row_loss = torch.empty((R,), dtype=torch.float32, device=logits.device) if targets is not None else None
+    loss = torch.empty((1,), dtype=torch.float32, device=logits.device) if targets is not None else None
+    st = lib().cattn_sce_fwd(_ptr(logits), _ptr(targets), _ptr(lse), _ptr(row_loss), _ptr(loss), R, V,
+                             _stream(logits.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_sce_fwd", last_error_string())
+    return lse, row_loss, loss
+
+
+def sce_bwd(logits, targets, lse, scale: float):
+    """dlogits = scale * (softmax(logits) - onehot(targets)), softmax recomputed from the saved lse."""
+    _f32_on_device("logits", logits)
+    R, V = _rows_cols(logits)
+    targets = _targets(targets, R, logits.device)
+    if targets is None:
+        raise ValueError("sce_bwd needs targets")
+    _f32_on_device("lse", lse, (R,))
+    dz = torch.empty_like(logits)
+    st = lib().cattn_sce_bwd(_ptr(logits), _ptr(targets), _ptr(lse), float(scale), _ptr(dz), R, V,
+                             _stream(logits.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_sce_bwd", last_error_string())
+    return dz

@@ -203,6 +203,18 @@ __device__ __forceinline__ float halves_sum(float x) { float a, b; halves(x, a, 
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Wave-wide maximum / sum over 64 lanes in a fixed pattern (every lane gets the result).
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) x += __shfl_xor(x, d, 64);
+  return x;
+}
+
 // Store 4 consecutive row elements (one accumulator run) converted to T.
 template <typename T> __device__ __forceinline__ void store4(T* dst, float a, float b, float c, float d);
 template <> __device__ __forceinline__ void store4<float>(float* dst, float a, float b, float c, float d) {

@@ -10,6 +10,7 @@
 #include "../../include/cattn.h"
 #include "attn_launch.h"
 #include "lmhead_launch.h"
+#include "memops_launch.h"
 
 extern "C" size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D);
 
@@ -58,6 +59,19 @@ cattn_status hip_status(hipError_t e) {
   if (e == hipSuccess) return CATTN_OK;
   snprintf(g_last_error, sizeof(g_last_error), "HIP error %d: %s", (int)e, hipGetErrorString(e));
   return CATTN_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// Every output range against every input range and against the other outputs.
+bool any_overlap(const Range* ins, int ni, const Range* outs, int no) {
+  for (int i = 0; i < no; ++i) {
+    for (int j = 0; j < ni; ++j)
+      if (overlap(outs[i], ins[j])) return true;
+    for (int j = i + 1; j < no; ++j)
+      if (overlap(outs[i], outs[j])) return true;
+  }
+  return false;
 }
 
 }  // namespace
@@ -209,6 +223,118 @@ cattn_status cattn_lmhead_fwd(const void* x, const void* w, const int* targets, 
   cattn::LmheadArgs a{x, w, targets, logits, lse, row_loss, targets ? loss : nullptr, workspace, M, N, K};
   (void)hipGetLastError();
   return hip_status(cattn::launch_lmhead(a, (hipStream_t)stream));
+}
+
+cattn_status cattn_layernorm_fwd(const float* x, const float* gamma, const float* beta, float* y, float* mean,
+                                 float* rstd, int rows, int C, float eps, void* stream) {
+  g_last_error[0] = '\0';
+  if (rows < 0 || C < 0) return fail(CATTN_ERR_INVALID_ARG, "negative rows or C");
+  if (!(eps >= 0.f) || !isfinite(eps)) return fail(CATTN_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (rows == 0 || C == 0) return CATTN_OK;
+  if (C % 4 || C > cattn::kLnMaxC) return fail(CATTN_ERR_UNSUPPORTED, "C must be a multiple of 4 and at most 4096");
+  if (!x || !gamma || !beta || !y || !mean || !rstd) return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  for (const void* p : {(const void*)x, (const void*)gamma, (const void*)beta, (const void*)y, (const void*)mean,
+                        (const void*)rstd})
+    if (!aligned16(p)) return fail(CATTN_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  const size_t n = (size_t)rows * C * 4;
+  const Range ins[3] = {range_of(x, n), range_of(gamma, (size_t)C * 4), range_of(beta, (size_t)C * 4)};
+  const Range outs[3] = {range_of(y, n), range_of(mean, (size_t)rows * 4), range_of(rstd, (size_t)rows * 4)};
+  if (any_overlap(ins, 3, outs, 3)) return fail(CATTN_ERR_INVALID_ARG, "outputs overlap inputs or each other");
+  (void)hipGetLastError();
+  return hip_status(cattn::launch_layernorm_fwd(x, gamma, beta, y, mean, rstd, rows, C, eps, (hipStream_t)stream));
+}
+
+size_t cattn_layernorm_bwd_workspace_bytes(int rows, int C) {
+  if (rows <= 0 || C <= 0) return 0;
+  return (size_t)cattn::ln_bwd_groups(rows) * 2 * (size_t)C * sizeof(float);
+}
+
+cattn_status cattn_layernorm_bwd(const float* x, const float* gamma, const float* mean, const float* rstd,
+                                 const float* dy, float* dx, float* dgamma, float* dbeta, float* workspace, int rows,
+                                 int C, void* stream) {
+  g_last_error[0] = '\0';
+  if (rows < 0 || C < 0) return fail(CATTN_ERR_INVALID_ARG, "negative rows or C");
+  if (rows == 0 || C == 0) return CATTN_OK;
+  if (C % 4 || C > cattn::kLnMaxC) return fail(CATTN_ERR_UNSUPPORTED, "C must be a multiple of 4 and at most 4096");
+  if (!x || !gamma || !mean || !rstd || !dy || !dx || !dgamma || !dbeta || !workspace)
+    return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  for (const void* p : {(const void*)x, (const void*)gamma, (const void*)mean, (const void*)rstd, (const void*)dy,
+                        (const void*)dx, (const void*)dgamma, (const void*)dbeta, (const void*)workspace})
+    if (!aligned16(p)) return fail(CATTN_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  const size_t n = (size_t)rows * C * 4;
+  const Range ins[5] = {range_of(x, n), range_of(gamma, (size_t)C * 4), range_of(mean, (size_t)rows * 4),
+                        range_of(rstd, (size_t)rows * 4), range_of(dy, n)};
+  const Range outs[4] = {range_of(dx, n), range_of(dgamma, (size_t)C * 4), range_of(dbeta, (size_t)C * 4),
+                         range_of(workspace, cattn_layernorm_bwd_workspace_bytes(rows, C))};
+  if (any_overlap(ins, 5, outs, 4)) return fail(CATTN_ERR_INVALID_ARG, "outputs overlap inputs or each other");
+  (void)hipGetLastError();
+  return hip_status(cattn::launch_layernorm_bwd(x, gamma, mean, rstd, dy, dx, dgamma, dbeta, workspace, rows, C,
+                                                (hipStream_t)stream));
+}
+
+static cattn_status gelu_common(const float* x, const float* dy, float* out, long long n, bool bwd, void* stream) {
+  g_last_error[0] = '\0';
+  if (n < 0) return fail(CATTN_ERR_INVALID_ARG, "negative n");
+  if (n == 0) return CATTN_OK;
+  if (n > (1LL << 40)) return fail(CATTN_ERR_UNSUPPORTED, "n exceeds 2^40");
+  if (!x || !out || (bwd && !dy)) return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  if (!aligned16(x) || !aligned16(out) || (bwd && !aligned16(dy)))
+    return fail(CATTN_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  const size_t b = (size_t)n * 4;
+  const Range ins[2] = {range_of(x, b), range_of(dy, bwd ? b : 0)};
+  const Range outs[1] = {range_of(out, b)};
+  if (any_overlap(ins, bwd ? 2 : 1, outs, 1)) return fail(CATTN_ERR_INVALID_ARG, "output overlaps an input");
+  (void)hipGetLastError();
+  return hip_status(cattn::launch_gelu(x, dy, out, (int64_t)n, bwd, (hipStream_t)stream));
+}
+
+cattn_status cattn_gelu_fwd(const float* x, float* y, long long n, void* stream) {
+  return gelu_common(x, nullptr, y, n, false, stream);
+}
+
+cattn_status cattn_gelu_bwd(const float* x, const float* dy, float* dx, long long n, void* stream) {
+  return gelu_common(x, dy, dx, n, true, stream);
+}
+
+cattn_status cattn_sce_fwd(const float* logits, const int* targets, float* lse, float* row_loss, float* loss, int rows,
+                           int V, void* stream) {
+  g_last_error[0] = '\0';
+  if (rows < 0 || V < 0) return fail(CATTN_ERR_INVALID_ARG, "negative rows or V");
+  if (rows == 0 || V == 0) return CATTN_OK;
+  if (V % 4) return fail(CATTN_ERR_UNSUPPORTED, "V must be a multiple of 4");
+  if (!logits || !lse || (targets && !row_loss)) return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  if (!targets) row_loss = loss = nullptr;
+  for (const void* p : {(const void*)logits, (const void*)targets, (const void*)lse, (const void*)row_loss,
+                        (const void*)loss})
+    if (!aligned16(p)) return fail(CATTN_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  const Range ins[2] = {range_of(logits, (size_t)rows * V * 4), range_of(targets, targets ? (size_t)rows * 4 : 0)};
+  const Range outs[3] = {range_of(lse, (size_t)rows * 4), range_of(row_loss, row_loss ? (size_t)rows * 4 : 0),
+                         range_of(loss, loss ? 4 : 0)};
+  if (any_overlap(ins, 2, outs, 3)) return fail(CATTN_ERR_INVALID_ARG, "outputs overlap inputs or each other");
+  (void)hipGetLastError();
+  hipError_t e = cattn::launch_sce_fwd(logits, targets, lse, row_loss, rows, V, (hipStream_t)stream);
+  if (e == hipSuccess && loss) e = cattn::launch_row_mean(row_loss, loss, rows, (hipStream_t)stream);
+  return hip_status(e);
+}
+
+cattn_status cattn_sce_bwd(const float* logits, const int* targets, const float* lse, float scale, float* dlogits,
+                           int rows, int V, void* stream) {
+  g_last_error[0] = '\0';
+  if (rows < 0 || V < 0) return fail(CATTN_ERR_INVALID_ARG, "negative rows or V");
+  if (!isfinite(scale)) return fail(CATTN_ERR_INVALID_ARG, "scale must be finite");
+  if (rows == 0 || V == 0) return CATTN_OK;
+  if (V % 4) return fail(CATTN_ERR_UNSUPPORTED, "V must be a multiple of 4");
+  const int64_t chunks = ((int64_t)V / 4 + 1023) / 1024;
+  if ((int64_t)rows * chunks >= (int64_t(1) << 31)) return fail(CATTN_ERR_UNSUPPORTED, "grid too large");
+  if (!logits || !targets || !lse || !dlogits) return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  for (const void* p : {(const void*)logits, (const void*)targets, (const void*)lse, (const void*)dlogits})
+    if (!aligned16(p)) return fail(CATTN_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  const size_t n = (size_t)rows * V * 4;
+  const Range ins[3] = {range_of(logits, n), range_of(targets, (size_t)rows * 4), range_of(lse, (size_t)rows * 4)};
+  const Range outs[1] = {range_of(dlogits, n)};
+  if (any_overlap(ins, 3, outs, 1)) return fail(CATTN_ERR_INVALID_ARG, "output overlaps an input");
+  (void)hipGetLastError();
+  return hip_status(cattn::launch_sce_bwd(logits, targets, lse, scale, dlogits, rows, V, (hipStream_t)stream));
 }
 
 size_t cattn_bwd_workspace_bytes(int B, int H, int S, int D) {

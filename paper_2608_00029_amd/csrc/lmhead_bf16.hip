@@ -31,13 +31,15 @@
 // Kernel 2 (merge): one wave per token row combines the row's N/64 partials
 // with the rescale-by-maximum-difference rule (the merge is not the fold),
 // giving LSE, and with a target id the row loss LSE - Z[row, target].
-// Kernel 3 (mean): one work group sums the M row losses in a fixed order.
+// Kernel 3 (mean, shared with the cross-entropy operator): one work group
+// sums the M row losses in a fixed order.
 #include <math.h>
 
 #include "attn_device.h"
 #include "bf16_stream.h"
 #include "lmhead_launch.h"
 #include "lmhead_sched.h"
+#include "memops_launch.h"
 
 namespace cattn {
 
@@ -160,18 +162,6 @@ __global__ __launch_bounds__(512) void lmhead_logits_stats_kernel(const bf16* __
   }
 }
 
-// Wave-wide maximum / sum over 64 lanes in a fixed pattern (every lane gets the result).
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
-  return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) x += __shfl_xor(x, d, 64);
-  return x;
-}
-
 // One wave per row: merge the row's partials (maximum, sum) into LSE; with
 // targets, the row's loss LSE - Z[row, target].
 __global__ __launch_bounds__(256) void lmhead_merge_kernel(const float* __restrict__ part,
@@ -199,21 +189,6 @@ __global__ __launch_bounds__(256) void lmhead_merge_kernel(const float* __restri
   }
 }
 
-// One work group: mean of the M row losses, summed in a fixed order.
-__global__ __launch_bounds__(256) void lmhead_mean_kernel(const float* __restrict__ row_loss, float* __restrict__ loss,
-                                                          int M) {
-  __shared__ float red[256];
-  float s = 0.f;
-  for (int i = threadIdx.x; i < M; i += 256) s += row_loss[i];
-  red[threadIdx.x] = s;
-  __syncthreads();
-  for (int d = 128; d > 0; d >>= 1) {
-    if ((int)threadIdx.x < d) red[threadIdx.x] += red[threadIdx.x + d];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) loss[0] = red[0] / (float)M;
-}
-
 // Work groups per chiplet of the persistent projection grid: one per compute
 // unit (the kernel's 128 KB of LDS allows no more).
 static int lmh_per_xcd() {
@@ -238,8 +213,7 @@ hipError_t launch_lmhead(const LmheadArgs& a, hipStream_t st) {
                      (const float*)a.logits, a.targets, a.lse, a.row_loss, a.M, a.N);
   e = hipGetLastError();
   if (e != hipSuccess || !a.targets || !a.loss) return e;
-  hipLaunchKernelGGL(lmhead_mean_kernel, dim3(1), dim3(256), 0, st, (const float*)a.row_loss, a.loss, a.M);
-  return hipGetLastError();
+  return launch_row_mean(a.row_loss, a.loss, a.M, st);
 }
 
 }  // namespace cattn

@@ -1,17 +1,19 @@
-"""Seeded synthetic inputs for the attention workloads.
+"""Seeded synthetic inputs for the attention, loss-head and memory-bound
+operator workloads.
 
-This module only draws random numbers; it holds none of attention's
+This module only draws random numbers; it holds none of the operators'
 arithmetic, and both the HIP path's callers and the CPU reference's callers
 take their inputs from here.
 
-Recipe (identical for every caller): a CPU ``torch.Generator`` seeded with
+Attention recipe (identical for every caller): a CPU ``torch.Generator`` seeded with
 ``seed`` draws float32 ``randn`` tensors of shape [B, H, S, D] in the order
 Q, K, V, dO; Q and K are then multiplied by ``qk_sigma``; for bf16 workloads
 every tensor is rounded to bfloat16 (round-to-nearest-even, torch's ``.to``).
 The values stand in for the attention activations of GPT-2 124M training
 (12 heads of dimension 64 at a 1024-token context, the model of the paper's
 Table 4, at the batch of 8 sequences its section 6.1 says it trains with);
-the paper's training data is not used.
+the paper's training data is not used.  The loss-head and memory-bound
+operator generators below state their own recipes.
 """
 
 from __future__ import annotations
@@ -131,3 +133,56 @@ def make_lmhead_inputs(M: int, N: int, K: int, w_sigma: float = 0.02, seed: int 
     y = torch.randint(0, N, (M,), generator=g, dtype=torch.int64).to(torch.int32)
     return x.contiguous(), w.contiguous(), y.contiguous()
 
+
+@dataclass(frozen=True)
+class MemopsWorkload:
+    """A memory-bound operator at the shape the paper measures it: LayerNorm over
+    [rows, C], GELU over rows * C elements, softmax cross entropy over [rows, C]
+    logits (C = vocabulary).  float32 tensors."""
+    name: str
+    op: str        # "layernorm", "gelu" or "sce"
+    rows: int
+    C: int
+    seed: int
+
+
+# The paper's memory-bound operator shapes (section 6, "Memory-Bound
+# Operators"): 16 sequences of 1024 tokens with GPT-2's width 768 (LayerNorm),
+# its MLP width 3072 (GELU) and its padded vocabulary 50304 (cross entropy).
+MEMOPS_WORKLOADS = [
+    MemopsWorkload("layernorm_16x1024x768", "layernorm", 16 * 1024, 768, SEED_BASE + 30),
+    MemopsWorkload("gelu_16x1024x3072", "gelu", 16 * 1024, 3072, SEED_BASE + 31),
+    MemopsWorkload("sce_16x1024x50304", "sce", 16 * 1024, 50304, SEED_BASE + 32),
+]
+
+GPT2_VOCAB = 50257  # real entries of the padded 50304-wide vocabulary
+
+
+def make_layernorm_inputs(rows: int, C: int, seed: int = SEED_BASE):
+    """(x [rows, C], gamma [C], beta [C], dy [rows, C]) float32 CPU tensors, drawn in that order:
+    x ~ N(0, 1) + 0.5 (residual-stream activations with a row offset the mean removes),
+    gamma ~ 1 + 0.1 N(0, 1), beta ~ 0.1 N(0, 1), dy ~ N(0, 1)."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    x = torch.randn((rows, C), generator=g, dtype=torch.float32) + 0.5
+    gamma = 1.0 + 0.1 * torch.randn((C,), generator=g, dtype=torch.float32)
+    beta = 0.1 * torch.randn((C,), generator=g, dtype=torch.float32)
+    dy = torch.randn((rows, C), generator=g, dtype=torch.float32)
+    return x.contiguous(), gamma.contiguous(), beta.contiguous(), dy.contiguous()
+
+
+def make_gelu_inputs(n: int, seed: int = SEED_BASE, sigma: float = 2.0):
+    """(x [n], dy [n]) float32 CPU tensors: x ~ N(0, sigma^2) (MLP pre-activations; sigma 2 reaches
+    both saturated tails of the tanh), dy ~ N(0, 1)."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    x = torch.randn((n,), generator=g, dtype=torch.float32) * sigma
+    dy = torch.randn((n,), generator=g, dtype=torch.float32)
+    return x.contiguous(), dy.contiguous()
+
+
+def make_sce_inputs(rows: int, V: int, seed: int = SEED_BASE, sigma: float = 2.0, n_real: int = 0):
+    """(logits [rows, V] float32, targets [rows] int32) CPU tensors: logits ~ N(0, sigma^2), targets
+    uniform over the first n_real entries (the real vocabulary; all V when n_real is 0)."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    z = torch.randn((rows, V), generator=g, dtype=torch.float32) * sigma
+    t = torch.randint(0, n_real or V, (rows,), generator=g, dtype=torch.int64).to(torch.int32)
+    return z.contiguous(), t.contiguous()

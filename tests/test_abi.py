@@ -164,3 +164,56 @@ def test_lmhead_argument_errors(lib):
     assert call(x, w, y, z, vp(P[3] + 64), rl, loss, ws) == b.CATTN_ERR_INVALID_ARG  # lse inside logits
     assert call(x, w, y, z, lse, rl, loss, vp(P[1] + 4)) == b.CATTN_ERR_INVALID_ARG  # workspace inside w
     assert "overlap" in b.last_error_string()
+
+
+def test_memops_argument_errors(lib):
+    vp, ll = ctypes.c_void_p, ctypes.c_longlong
+    p = [vp(a) for a in P]
+    s0 = vp(0)
+    # LayerNorm forward
+    assert lib.cattn_layernorm_fwd(*p[:6], -1, 768, 1e-5, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_layernorm_fwd(*p[:6], 16, 768, -1.0, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_layernorm_fwd(*p[:6], 16, 768, float("nan"), s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_layernorm_fwd(*[vp(0)] * 6, 0, 768, 1e-5, s0) == b.CATTN_OK  # empty
+    assert lib.cattn_layernorm_fwd(*p[:6], 16, 770, 1e-5, s0) == b.CATTN_ERR_UNSUPPORTED
+    assert lib.cattn_layernorm_fwd(*p[:6], 16, 4100, 1e-5, s0) == b.CATTN_ERR_UNSUPPORTED
+    assert lib.cattn_layernorm_fwd(vp(0), *p[1:6], 16, 768, 1e-5, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_layernorm_fwd(vp(P[0] + 4), *p[1:6], 16, 768, 1e-5, s0) == b.CATTN_ERR_INVALID_ARG  # alignment
+    assert lib.cattn_layernorm_fwd(p[0], p[1], p[2], p[0], p[4], p[5], 16, 768, 1e-5, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_layernorm_fwd(*p[:4], vp(P[3] + 16), p[5], 16, 768, 1e-5, s0) == b.CATTN_ERR_INVALID_ARG
+    # LayerNorm backward
+    assert lib.cattn_layernorm_bwd(*p[:8], vp(0), 16, 768, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_layernorm_bwd(*p[:8], vp(P[4] + 32), 16, 768, s0) == b.CATTN_ERR_INVALID_ARG  # ws inside dy
+    assert lib.cattn_layernorm_bwd(*p[:9], 16, 6, s0) == b.CATTN_ERR_UNSUPPORTED
+    assert lib.cattn_layernorm_bwd(*[vp(0)] * 9, 16, 0, s0) == b.CATTN_OK
+    assert b.layernorm_bwd_workspace_bytes(16384, 768) == 512 * 2 * 768 * 4
+    assert b.layernorm_bwd_workspace_bytes(20, 768) == 2 * 2 * 768 * 4
+    assert b.layernorm_bwd_workspace_bytes(0, 768) == 0
+    # GELU
+    assert lib.cattn_gelu_fwd(p[0], p[1], ll(-1), s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_gelu_fwd(vp(0), vp(0), ll(0), s0) == b.CATTN_OK
+    assert lib.cattn_gelu_fwd(p[0], p[0], ll(1024), s0) == b.CATTN_ERR_INVALID_ARG      # in place
+    assert lib.cattn_gelu_bwd(p[0], p[1], vp(P[1] + 64), ll(1024), s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_gelu_bwd(p[0], vp(0), p[2], ll(1024), s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_gelu_fwd(vp(P[0] + 8), p[1], ll(1024), s0) == b.CATTN_ERR_INVALID_ARG
+    # softmax cross entropy
+    assert lib.cattn_sce_fwd(*p[:5], 16, 50302, s0) == b.CATTN_ERR_UNSUPPORTED
+    assert lib.cattn_sce_fwd(*p[:5], -2, 50304, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_sce_fwd(p[0], p[1], p[2], vp(0), p[4], 16, 50304, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_sce_fwd(p[0], p[1], vp(P[0] + 64), p[3], p[4], 16, 50304, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_sce_fwd(*[vp(0)] * 5, 0, 50304, s0) == b.CATTN_OK
+    assert lib.cattn_sce_bwd(*p[:3], ctypes.c_float(float("inf")), p[3], 16, 50304, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_sce_bwd(p[0], vp(0), p[2], ctypes.c_float(1.0), p[3], 16, 50304, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_sce_bwd(*p[:3], ctypes.c_float(1.0), p[0], 16, 50304, s0) == b.CATTN_ERR_INVALID_ARG
+    assert lib.cattn_sce_bwd(*p[:3], ctypes.c_float(1.0), p[3], 16, 10, s0) == b.CATTN_ERR_UNSUPPORTED
+
+
+def test_memops_binding_refuses_cpu_tensors(lib):
+    import torch
+    x = torch.zeros(4, 8)
+    with pytest.raises(ValueError):
+        b.gelu_fwd(x)
+    with pytest.raises(ValueError):
+        b.layernorm_fwd(x, torch.ones(8), torch.zeros(8))
+    with pytest.raises(ValueError):
+        b.sce_fwd(x)
