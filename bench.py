@@ -13,8 +13,10 @@ kernel's mean duration over those launches gives the roofline entry.  After
 the timed region every workload (the tiny float32 one, GPT-2 small/medium, XL
 width, long context, and GPT-2 small stored [B, S, H, D]) is timed too --
 forward, backward and whole step -- under "configs", and shapes across the
-paper's attention sweep under "sweep" (--configs 0 skips both; profile runs
-do).  On
+paper's attention sweep under "sweep", the fused loss head under "lmhead" and
+the memory-bound operators (LayerNorm, GELU, softmax cross entropy, forward
+and backward, with their HBM bandwidth) under "memops" (--configs 0 skips
+all of these).  On
 rank 0 the float64 CPU oracle is then timed on a bounded sample of the same
 workload (whole (batch, head) slices) as a reported baseline.  Prints ONE JSON
 line.
@@ -215,6 +217,81 @@ def time_lmhead(wl, bd, steps: int, warmup: int):
                          "hbm": round(nbytes / (HBM_PEAK_GBS * 1e9) * 1e6, 1)}}
 
 
+def time_memops(wl, bd, steps: int, warmup: int):
+    """One memory-bound operator (LayerNorm, GELU or softmax cross entropy) at
+    the paper's shape, forward and backward, inputs resident in HBM: mean ms per
+    call over `steps` calls each, timed with HIP events on the stream the
+    kernels run on.  Bandwidth is reported twice: over the algorithmic bytes
+    (every input read once, every output written once, workspace partials
+    written and read once) against the 8 TB/s HBM peak, and over the paper's
+    own byte counts (one read and one write of the activation for LayerNorm and
+    GELU, one read of the logits for the cross-entropy forward, a read and a
+    write of the vocabulary-sized gradient for its backward)."""
+    import ctypes
+    import torch
+    from paper_2608_00029_amd import workloads as W
+    dev = torch.device("cuda:0")
+    L = bd.lib()
+    sp = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    R, C = wl.rows, wl.C
+    f32 = dict(dtype=torch.float32, device=dev)
+
+    def checked(name, st):
+        if st != 0:
+            raise RuntimeError(f"{wl.name} {name}: {bd.last_error_string()}")
+
+    # raw C-ABI calls on preallocated buffers, so that the host enqueues faster than the GPU drains
+    if wl.op == "layernorm":
+        x, g, be, dy = (t.to(dev) for t in W.make_layernorm_inputs(R, C, wl.seed))
+        y, dx = torch.empty_like(x), torch.empty_like(x)
+        mean, rstd, dg, db = torch.empty(R, **f32), torch.empty(R, **f32), torch.empty(C, **f32), torch.empty(C, **f32)
+        ws = torch.empty((bd.layernorm_bwd_workspace_bytes(R, C) // 4,), **f32)
+        p_fwd = [t.data_ptr() for t in (x, g, be, y, mean, rstd)]
+        p_bwd = [t.data_ptr() for t in (x, g, mean, rstd, dy, dx, dg, db, ws)]
+        fwd = lambda: checked("fwd", L.cattn_layernorm_fwd(*p_fwd, R, C, ctypes.c_float(1e-5), sp))
+        bwd = lambda: checked("bwd", L.cattn_layernorm_bwd(*p_bwd, R, C, sp))
+        n_ws = ws.numel() * 4
+        alg = (8 * R * C + 8 * C + 8 * R, 12 * R * C + 8 * R + 12 * C + 2 * n_ws)
+        paper = (8 * R * C, 8 * R * C)
+    elif wl.op == "gelu":
+        n = R * C
+        x, dy = (t.to(dev) for t in W.make_gelu_inputs(n, wl.seed))
+        y = torch.empty_like(x)
+        fwd = lambda: checked("fwd", L.cattn_gelu_fwd(x.data_ptr(), y.data_ptr(), n, sp))
+        bwd = lambda: checked("bwd", L.cattn_gelu_bwd(x.data_ptr(), dy.data_ptr(), y.data_ptr(), n, sp))
+        alg = (8 * n, 12 * n)
+        paper = (8 * n, 8 * n)
+    else:
+        z, t = (a.to(dev) for a in W.make_sce_inputs(R, C, wl.seed, n_real=W.GPT2_VOCAB))
+        lse, rl, loss = torch.empty(R, **f32), torch.empty(R, **f32), torch.empty(1, **f32)
+        dz = torch.empty_like(z)
+        p_fwd = [a.data_ptr() for a in (z, t, lse, rl, loss)]
+        fwd = lambda: checked("fwd", L.cattn_sce_fwd(*p_fwd, R, C, sp))
+        bwd = lambda: checked("bwd", L.cattn_sce_bwd(z.data_ptr(), t.data_ptr(), lse.data_ptr(),
+                                                     ctypes.c_float(1.0 / R), dz.data_ptr(), R, C, sp))
+        alg = (4 * R * C + 16 * R + 4, 8 * R * C + 8 * R)
+        paper = (4 * R * C, 8 * R * C)
+    fwd()  # the backward reads what the forward writes (mean / rstd, lse)
+    out = {"rows": R, "C": C}
+    stream = torch.cuda.current_stream(dev)
+    torch.cuda.synchronize()
+    for name, f, ab, nb in (("fwd", fwd, alg[0], paper[0]), ("bwd", bwd, alg[1], paper[1])):
+        for _ in range(warmup):
+            f()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        gbs = ab / (ms * 1e-3) / 1e9
+        out[name] = {"ms": round(ms, 5), "gbs_algorithmic": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 3),
+                     "gbs_paper_bytes": round(nb / (ms * 1e-3) / 1e9, 1), "bytes_algorithmic": ab}
+    return out
+
+
 def copy_probe(mib: int) -> int:
     """A plain copy of known size: it reads and writes exactly mib MiB per launch."""
     import torch
@@ -355,6 +432,8 @@ def main() -> int:
         line["sweep"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in SWEEP}
         from paper_2608_00029_amd.workloads import LMHEAD_WORKLOADS
         line["lmhead"] = {c.name: time_lmhead(c, bd, steps=20, warmup=3) for c in LMHEAD_WORKLOADS}
+        from paper_2608_00029_amd.workloads import MEMOPS_WORKLOADS
+        line["memops"] = {c.name: time_memops(c, bd, steps=20, warmup=3) for c in MEMOPS_WORKLOADS}
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, cpu_inputs, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -6,7 +6,9 @@
 // All of them move far more bytes than they compute on, so the design is about
 // HBM: every access is a 16-byte vector load or store by consecutive lanes
 // (a wave moves 1 KB per instruction), each thread keeps several loads in
-// flight before it uses any of them, intermediate values stay in registers
+// flight before it uses any of them, outputs and the streams read once are
+// accessed non-temporally (where that measured faster on the MI355X: all
+// stores, the loads of the GELU backward and of both cross-entropy kernels), intermediate values stay in registers
 // (the softmax of the cross-entropy backward is recomputed from the logits and
 // the saved LSE, never stored), and reductions are done in a fixed order so
 // that results are bitwise reproducible.
@@ -71,8 +73,12 @@ __global__ __launch_bounds__(256) void gelu_kernel(const float* __restrict__ x, 
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t i = i0 + u * 256;
       if (i < n4) {
-        v[u] = x4[i];
-        if constexpr (BWD) g[u] = g4[i];
+        if constexpr (BWD) {
+          v[u] = __builtin_nontemporal_load(&x4[i]);
+          g[u] = __builtin_nontemporal_load(&g4[i]);
+        } else {
+          v[u] = x4[i];
+        }
       }
     }
 #pragma unroll
@@ -82,7 +88,7 @@ __global__ __launch_bounds__(256) void gelu_kernel(const float* __restrict__ x, 
         f32x4 r;
 #pragma unroll
         for (int e = 0; e < 4; ++e) r[e] = BWD ? g[u][e] * gelu_dydx(v[u][e]) : gelu_y(v[u][e]);
-        o4[i] = r;
+        __builtin_nontemporal_store(r, &o4[i]);
       }
     }
   }
@@ -133,7 +139,7 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* __restr
     f32x4* yr = (f32x4*)(y + (int64_t)row * C);
 #pragma unroll
     for (int k = 0; k < NPL; ++k)
-      if (lane + 64 * k < C4) yr[lane + 64 * k] = (v[k] - mu) * rs * g[k] + b[k];
+      if (lane + 64 * k < C4) __builtin_nontemporal_store((v[k] - mu) * rs * g[k] + b[k], &yr[lane + 64 * k]);
     if (lane == 0) {
       mean[row] = mu;
       rstd[row] = rs;
@@ -188,7 +194,7 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* __restr
 #pragma unroll
     for (int k = 0; k < NPL; ++k)
       if (lane + 64 * k < C4) {
-        dxr[lane + 64 * k] = rs * (d[k] * g[k] - a - v[k] * c2);
+        __builtin_nontemporal_store(rs * (d[k] * g[k] - a - v[k] * c2), &dxr[lane + 64 * k]);
         dg[k] += d[k] * v[k];
         db[k] += d[k];
       }
@@ -211,24 +217,30 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* __restr
   for (int c = threadIdx.x; c < 2 * C4; c += 256) pr[c] = red[c];
 }
 
-// dgamma / dbeta: column quad q = blockIdx.x * 64 + lane of the 2C/4 quads of a
-// partial row; wave w sums partial rows w, w + 16, ...; then wave 0 adds the
-// 16 wave sums in order.
+// dgamma / dbeta: work group k sums column quads 8k .. 8k+7 of the 2C/4 quads
+// of a partial row over all partial rows.  Lane l of wave w takes quad
+// 8k + (l & 7) of partial rows j, j + 128, ... with j = 8w + (l >> 3), so a
+// thread issues all its loads at once; the eight row streams of a wave are
+// then added by a fixed butterfly, and wave 0 adds the 16 wave sums in order.
 __global__ __launch_bounds__(1024) void layernorm_bwd_reduce_kernel(const float* __restrict__ part,
                                                                     float* __restrict__ dgamma,
                                                                     float* __restrict__ dbeta, int n_part, int C) {
-  __shared__ f32x4 red[16][64];
+  __shared__ f32x4 red[16][8];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int C4 = C >> 2, q = blockIdx.x * 64 + lane;
+  const int C4 = C >> 2, q = blockIdx.x * 8 + (lane & 7);
   const bool ok = q < 2 * C4;
   f32x4 s = f32x4{};
   if (ok) {
     const f32x4* p4 = (const f32x4*)part;
-    for (int i = w; i < n_part; i += 16) s += p4[(int64_t)i * 2 * C4 + q];
+    for (int i = 8 * w + (lane >> 3); i < n_part; i += 128) s += p4[(int64_t)i * 2 * C4 + q];
   }
-  red[w][lane] = s;
+#pragma unroll
+  for (int d = 8; d < 64; d <<= 1)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[e] += __shfl_xor(s[e], d, 64);
+  if (lane < 8) red[w][lane] = s;
   __syncthreads();
-  if (w == 0 && ok) {
+  if (w == 0 && lane < 8 && ok) {
     f32x4 t = red[0][lane];
     for (int i = 1; i < 16; ++i) t += red[i][lane];
     if (q < C4)
@@ -258,7 +270,7 @@ __global__ __launch_bounds__(256) void sce_fwd_kernel(const float* __restrict__ 
     f32x4 v[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u)
-      if (i0 + u * 256 < V4) v[u] = zr[i0 + u * 256];
+      if (i0 + u * 256 < V4) v[u] = __builtin_nontemporal_load(&zr[i0 + u * 256]);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u)
       if (i0 + u * 256 < V4) {
@@ -307,7 +319,7 @@ __global__ __launch_bounds__(256) void sce_bwd_kernel(const float* __restrict__ 
   f32x4 v[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u)
-    if (i0 + u * 256 < V4) v[u] = zr[i0 + u * 256];
+    if (i0 + u * 256 < V4) v[u] = __builtin_nontemporal_load(&zr[i0 + u * 256]);
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     const int i = i0 + u * 256;
@@ -320,18 +332,26 @@ __global__ __launch_bounds__(256) void sce_bwd_kernel(const float* __restrict__ 
       } else if ((t >> 2) == i) {
         p[t & 3] -= 1.f;
       }
-      dr[i] = p * scale;
+      __builtin_nontemporal_store(p * scale, &dr[i]);
     }
   }
 }
 
-__global__ __launch_bounds__(256) void row_mean_kernel(const float* __restrict__ v, float* __restrict__ loss, int M) {
-  __shared__ float red[256];
+// Mean of M floats: thread i sums v[i], v[i + 1024], ... (loads issued four at
+// a time), then a fixed tree over the 1024 partial sums.
+__global__ __launch_bounds__(1024) void row_mean_kernel(const float* __restrict__ v, float* __restrict__ loss, int M) {
+  __shared__ float red[1024];
   float s = 0.f;
-  for (int i = threadIdx.x; i < M; i += 256) s += v[i];
+  for (int i0 = threadIdx.x; i0 < M; i0 += 4096) {
+    float a[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) a[u] = i0 + 1024 * u < M ? v[i0 + 1024 * u] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s += a[u];
+  }
   red[threadIdx.x] = s;
   __syncthreads();
-  for (int d = 128; d > 0; d >>= 1) {
+  for (int d = 512; d > 0; d >>= 1) {
     if ((int)threadIdx.x < d) red[threadIdx.x] += red[threadIdx.x + d];
     __syncthreads();
   }
@@ -380,7 +400,7 @@ hipError_t launch_layernorm_bwd(const float* x, const float* gamma, const float*
 #undef LN_BWD
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layernorm_bwd_reduce_kernel, dim3((unsigned)((2 * (C / 4) + 63) / 64)), dim3(1024), 0, st,
+  hipLaunchKernelGGL(layernorm_bwd_reduce_kernel, dim3((unsigned)((2 * (C / 4) + 7) / 8)), dim3(1024), 0, st,
                      (const float*)part, dgamma, dbeta, groups, C);
   return hipGetLastError();
 }
@@ -412,7 +432,7 @@ hipError_t launch_sce_bwd(const float* z, const int* targets, const float* lse, 
 }
 
 hipError_t launch_row_mean(const float* v, float* loss, int M, hipStream_t st) {
-  hipLaunchKernelGGL(row_mean_kernel, dim3(1), dim3(256), 0, st, v, loss, M);
+  hipLaunchKernelGGL(row_mean_kernel, dim3(1), dim3(1024), 0, st, v, loss, M);
   return hipGetLastError();
 }
 

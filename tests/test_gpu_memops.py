@@ -9,8 +9,9 @@ Tolerances, derived from the float32 arithmetic of the kernels:
   |mean| and enters xhat multiplied by rstd, and dx itself scales with rstd.
   mean: |err| <= 1e-5 (|mean| + 1/rstd); rstd: relative 1e-5.  dgamma,
   dbeta: each is a sum over every row, accumulated in chains of at most ~100
-  float additions (a wave's rows, the four waves of a group, the 16-wave
-  column sums of the partial rows), so the error is bounded by
+  float additions (a wave's rows, the four waves of a group, then the partial
+  rows in 128 strided streams, a butterfly and 16 wave sums), so the error is
+  bounded by
   100 * 2^-24 * sum_r |term| < 1e-5 * sum_r |term|, which is the test.
 * GELU y: |err| <= 1e-6 (1 + |x|): y = x (1 - r) with r = 1 / (1 + 2^t) from
   one hardware exp2 and one reciprocal (1 ulp each) and t from three
