@@ -46,11 +46,17 @@ PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2608_00029_amd", "csrc")
 
 
-def kernel_source_digest() -> str:
-    """sha256 over the HIP kernel sources (names and bytes), so that a stored
-    counter measurement can be tied to the kernels it was taken on."""
+# Sources the attention kernels are compiled from (the loss head and the
+# memory-bound operators live in other files and do not change them).
+ATTN_SOURCES = ("attn_bf16.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_device.h", "attn_sched.h", "attn_launch.h",
+                "bf16_stream.h")
+
+
+def kernel_source_digest(names=ATTN_SOURCES) -> str:
+    """sha256 over the attention kernels' sources (names and bytes), so that a
+    stored counter measurement can be tied to the kernels it was taken on."""
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h"))):
+    for p in sorted(os.path.join(CSRC, n) for n in names):
         h.update(os.path.basename(p).encode())
         with open(p, "rb") as f:
             h.update(f.read())
