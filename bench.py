@@ -325,9 +325,10 @@ def main() -> int:
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark, run 5 plain device-to-device copies of this many MiB "
                          "(reference kernel for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
-    ap.add_argument("--memops-only", action="store_true",
+    ap.add_argument("--only", choices=("memops", "lmhead"), default=None,
                     help="instead of the benchmark, time only the memory-bound operators (forward and "
-                         "backward, --steps calls each) and print their JSON (for counter collection)")
+                         "backward) or only the fused loss head, --steps calls each after --warmup, and "
+                         "print their JSON (for counter collection)")
     args = ap.parse_args()
     if args.copy_probe_mib > 0:
         return copy_probe(args.copy_probe_mib)
@@ -345,10 +346,15 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py: no HIP device visible", file=sys.stderr)
         return 1
-    if args.memops_only:
+    if args.only == "memops":
         from paper_2608_00029_amd.workloads import MEMOPS_WORKLOADS
         print(json.dumps({c.name: time_memops(c, bd, steps=args.steps, warmup=args.warmup)
                           for c in MEMOPS_WORKLOADS}), flush=True)
+        return 0
+    if args.only == "lmhead":
+        from paper_2608_00029_amd.workloads import LMHEAD_WORKLOADS
+        print(json.dumps({c.name: time_lmhead(c, bd, steps=args.steps, warmup=args.warmup)
+                          for c in LMHEAD_WORKLOADS}), flush=True)
         return 0
     w = BY_NAME[args.workload]
     dev = torch.device("cuda:0")
