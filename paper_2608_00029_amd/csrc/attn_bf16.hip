@@ -54,6 +54,18 @@ namespace cattn {
 #ifndef CATTN_BAND  // rounds of work groups dealt in alternating directions (0: plain heaviest-first)
 #define CATTN_BAND cu_count()
 #endif
+#ifndef CATTN_DKDV_NB64  // dK/dV ring depth at D = 64 (unsplit)
+#define CATTN_DKDV_NB64 CATTN_BWD_NB64
+#endif
+#ifndef CATTN_DKDV_GROUP  // iterations per barrier of the unsplit rings (where the ring is deep enough)
+#define CATTN_DKDV_GROUP 2
+#endif
+#ifndef CATTN_DQ_GROUP
+#define CATTN_DQ_GROUP 2
+#endif
+#ifndef CATTN_FWD_GROUP
+#define CATTN_FWD_GROUP 2
+#endif
 #ifndef CATTN_DKDV_NB64S  // dQ and dK/dV at D = 64 with the loop range split in two (two rings)
 #define CATTN_DKDV_NB64S 4
 #endif
@@ -91,7 +103,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
                                                             float c, int band, int H, int seq_major) {
   typedef TileGeom<D> G;
   constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
-  constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
+  constexpr int TILE = G::TILE, SET = 2 * TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR;
   __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * SET];  // [part][slot][K, V]
@@ -144,13 +156,9 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       }
     }
   };
-  // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
   constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
-  auto later = [&](int i) { return ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE; };
-
-  unroll<AH>([&](auto I) {
-    if (decltype(I)::value < L) dma(decltype(I)::value, I);
-  });
+  constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_FWD_GROUP);  // iterations per barrier
+  ring_prologue<NB, GROUP>(L, dma);
   MB::frag qf[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
   wait_vm(0);
@@ -200,14 +208,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       constexpr int pc = PAR ? (sl & 1) : 0, pn = PAR ? (pc ^ 1) : 1;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
-        if (i + AH - 1 < n_last) {
-          tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
-        } else {
-          tile_barrier(later(i));
-        }
-      }
-      if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
+      ring_step<NB, GROUP, NEED, SPLIT, PER_TILE, sl>(i, L, n_last, dma);
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
       f32x16& sa_ = sa[pc];
       // causal diagonal / ragged end: only the last tile of the wave's queries
@@ -350,7 +351,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
                                                                float c, float scale, int band, int H, int seq_major) {
   typedef TileGeom<D> G;
   constexpr int QG = 4 / SPLIT, BQ = 32 * QG;
-  constexpr int AH = NB - 1, TILE = G::TILE, SET = 2 * TILE;
+  constexpr int TILE = G::TILE, SET = 2 * TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR;
   __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * SET];  // [part][slot][K, V]
@@ -403,12 +404,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
       }
     }
   };
-  // copies issued after iteration i+1's and still allowed in flight at the top of iteration i
   constexpr int NEED = 0;  // iteration i reads the tiles of iterations i .. i+NEED
-  auto later = [&](int i) { return ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE; };
-  unroll<AH>([&](auto I) {
-    if (decltype(I)::value < L) dma(decltype(I)::value, I);
-  });
+  constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_DQ_GROUP);  // iterations per barrier
+  ring_prologue<NB, GROUP>(L, dma);
   MB::frag qf[KS_D], dof[KS_D], of[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
   load_row_frags<bf16, D>(dO + base, my_q, S, h, rs, dof);
@@ -446,14 +444,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
       constexpr int sl = decltype(slc)::value;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
-        if (i + AH - 1 < n_last) {
-          tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
-        } else {
-          tile_barrier(later(i));
-        }
-      }
-      if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
+      ring_step<NB, GROUP, NEED, SPLIT, PER_TILE, sl>(i, L, n_last, dma);
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
       const int j = tb + i;  // key tile of this iteration
       const char* cur = ring + sl * SET;
@@ -553,7 +544,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
                                                                  int seq_major) {
   typedef TileGeom<D> G;
   constexpr int KG = 4 / SPLIT, BKV = 32 * KG;
-  constexpr int AH = NB - 1, TILE = G::TILE;
+  constexpr int TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
   constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats -LSE/scale, 32 floats D
   // copies per part tile issued by every wave: its share of Q and dO, and 4 of the 16 LSE/D chunks
@@ -596,7 +587,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const int t_rag = (S % 32) ? (S - 1) / 32 - jt0 : -1;                           // ragged tile (workgroup index)
   const int i_rag = t_rag - tb;                                                   // ... in this part
   // copies: iteration x of the ring holds tile p*L + x of every part p with x < L (x < n_last for the last)
-  const int x_full = n_last;  // iterations below this have a tile in every part
 
   TileCopy<D> tc;
   tc.init(w, lane, rs);
@@ -618,12 +608,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       }
     }
   };
-  // copies of this wave issued after iteration i+1's and still allowed in flight at the top of iteration i
   constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
-  auto later = [&](int i) { return ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE; };
-  unroll<AH>([&](auto I) {
-    if (decltype(I)::value < L) dma(decltype(I)::value, I);
-  });
+  // With one part, the waves meet at a barrier every GROUP iterations: a wave
+  // that runs late on its SIMD then holds the others back less often.
+  constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_DKDV_GROUP);
+  ring_prologue<NB, GROUP>(L, dma);
   MB::frag kf[KS_D], vf[KS_D];
   load_row_frags<bf16, D>(K + base, my_k, S, h, rs, kf);
   load_row_frags<bf16, D>(V + base, my_k, S, h, rs, vf);
@@ -646,14 +635,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       constexpr int sl = decltype(slc)::value, sn = (sl + 1) % NB;
       const int i = i0 + sl;
       if (i >= L) return;
-      if (i > 0) {  // the tiles this iteration reads landed; iteration i-1's slots are free
-        if (i + AH - 1 < x_full) {
-          tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
-        } else {
-          tile_barrier(later(i));
-        }
-      }
-      if (i + AH < L) dma(i + AH, IC<(sl + AH) % NB>{});
+      ring_step<NB, GROUP, NEED, SPLIT, PER_TILE, sl>(i, L, n_last, dma);
       if ((unsigned)(i - i_lo) >= (unsigned)i_span) return;  // wave-uniform: not an active sub-block
       const char* lq = ring + sl * BUF;
       const char* ldo = lq + TILE;
@@ -783,6 +765,7 @@ template <int D> struct FwdCfg {
 };
 template <int D> struct BwdCfg {
   static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_BWD_NB128;
+  static constexpr int NB_DKDV = D == 64 ? CATTN_DKDV_NB64 : CATTN_BWD_NB128;
 };
 
 template <int D, bool CAUSAL, int SPLIT, int NB>
@@ -856,7 +839,7 @@ static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   if constexpr (D == 64) {
     if (split) return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st);
   }
-  return launch_dkdv<D, CAUSAL, 1, NB>(a, c, st);
+  return launch_dkdv<D, CAUSAL, 1, BwdCfg<D>::NB_DKDV>(a, c, st);
 }
 
 hipError_t launch_bwd_bf16(const BwdArgs& a, int phase, hipStream_t st) {

@@ -52,5 +52,25 @@ constexpr int banded_rank(int bid, int n, int band) {
   return r * band + (size / kXcdGroup - 1 - p / kXcdGroup) * kXcdGroup + p % kXcdGroup;
 }
 
+// Ring with one barrier per group of G iterations (one part; G divides the
+// ring depth NB): the prologue copies tiles 0 .. NB-G-1, and at the top of
+// iteration i (i % G == 0) the copies of tiles i+NB-G .. i+NB-1 are issued
+// into the slots of tiles i-G .. i-1, which every wave finished at the
+// barrier.  Iterations i .. i+G-1 read tiles up to i+G-1+need, so the wait at
+// the top of i (i > 0) may leave in flight the tiles issued before that lie
+// beyond it: this is their number.  Needs NB >= 2 G + need (the tiles a
+// group reads are then copied before its top).
+// Iterations per barrier a ring of NB slots can take with `split` parts and
+// `need` tiles of look-ahead: `want` when grouping is possible (one part, NB
+// a multiple of it, NB >= 2 want + need), else 1.
+constexpr int ring_group(int split, int NB, int need, int want) {
+  return (want > 1 && split == 1 && NB % want == 0 && NB >= 2 * want + need) ? want : 1;
+}
+constexpr int ring_group_in_flight(int i, int L, int NB, int G, int need) {
+  const int last_issued = imin(L - 1, i + NB - G - 1);
+  const int d = last_issued - (i + G - 1 + need);
+  return d > 0 ? d : 0;
+}
+
 }  // namespace cattn
 

@@ -83,6 +83,48 @@ template <int N> __device__ __forceinline__ void tile_barrier_c() {
   asm volatile("s_barrier" ::: "memory");
 }
 
+// The ring protocol at the top of iteration i (ring slot SL = i % NB, every
+// part's tile x in slot x % NB): wait for the tiles this iteration (or group
+// of GROUP iterations) reads, meet the other waves, then copy the tiles the
+// slots freed by the barrier take next.  GROUP == 1: every iteration, tile
+// i + NB - 1 (ring_in_flight counts what may stay in flight); GROUP > 1: at
+// the first iteration of each group, tiles i + NB - GROUP .. i + NB - 1
+// (ring_group_in_flight).  dma(x, IC<slot>) copies iteration x's tiles;
+// every wave issues PER_TILE copies per tile and part.  The tiles before the
+// loop come from ring_prologue.
+template <int NB, int GROUP, int NEED, int SPLIT, int PER_TILE, int SL, typename Dma>
+__device__ __forceinline__ void ring_step(int i, int L, int n_last, Dma& dma) {
+  constexpr int AH = NB - 1;
+  if constexpr (GROUP == 1) {
+    if (i > 0) {
+      if (i + AH - 1 < n_last) {
+        tile_barrier_c<ring_in_flight_full(SPLIT, AH, NEED) * PER_TILE>();
+      } else {
+        tile_barrier(ring_in_flight(i, L, n_last, SPLIT, AH, NEED) * PER_TILE);
+      }
+    }
+    if (i + AH < L) dma(i + AH, IC<(SL + AH) % NB>{});
+  } else if constexpr (SL % GROUP == 0) {
+    static_assert(SPLIT == 1 && NB % GROUP == 0 && NB >= 2 * GROUP + NEED, "grouped ring");
+    if (i > 0) {
+      if (i + NB - 1 < L) {
+        tile_barrier_c<ring_group_in_flight(0, 1 << 20, NB, GROUP, NEED) * PER_TILE>();
+      } else {
+        tile_barrier(ring_group_in_flight(i, L, NB, GROUP, NEED) * PER_TILE);
+      }
+    }
+    unroll<GROUP>([&](auto g) {
+      constexpr int x = NB - GROUP + decltype(g)::value;
+      if (i + x < L) dma(i + x, IC<(SL + x) % NB>{});
+    });
+  }
+}
+template <int NB, int GROUP, typename Dma> __device__ __forceinline__ void ring_prologue(int L, Dma& dma) {
+  unroll<NB - GROUP>([&](auto I) {
+    if (decltype(I)::value < L) dma(decltype(I)::value, I);
+  });
+}
+
 // Byte address of an LDS location (the value M0 takes).
 __device__ __forceinline__ unsigned lds_addr(const char* p) {
   return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char*)p;

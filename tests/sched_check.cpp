@@ -85,6 +85,45 @@ int main() {
       }
     }
   }
+  // grouped ring (one barrier per G iterations): every tile an iteration reads has landed at the
+  // group's wait (copies complete in issue order), and no copy overwrites a tile still to be read
+  for (int NB : {3, 4, 6, 8, 9, 12}) {
+    for (int G : {1, 2, 3, 4})
+    for (int need : {0, 1}) {
+      const int pro = NB - G;
+      if (NB % G || NB < 2 * G + need || ring_group(1, NB, need, G) != G) continue;
+      for (int L = 1; L <= 70; ++L) {
+        std::vector<int> order;  // tiles in issue order
+        for (int t = 0; t < pro && t < L; ++t) order.push_back(t);
+        std::vector<char> landed(L, 0);
+        for (int t : order) landed[t] = 1;  // the prologue waits for everything
+        for (int i = 0; i < L; i += G) {
+          if (i > 0) {
+            const int k = ring_group_in_flight(i, L, NB, G, need);
+            ++checks;
+            if (k < 0 || k > (int)order.size()) {
+              ++bad;
+              continue;
+            }
+            for (size_t x = 0; x + k < order.size(); ++x) landed[order[x]] = 1;
+          }
+          for (int g = 0; g < G; ++g) {
+            const int t = i + pro + g;
+            if (t >= L) continue;
+            ++checks;
+            const int prev = t - NB;  // the slot's previous tile: read by iterations prev - 1 and prev
+            if (prev >= 0 && prev >= i) ++bad;
+            order.push_back(t);
+          }
+          for (int j = i; j < i + G && j < L; ++j)
+            for (int t = j; t <= j + need && t < L; ++t) {
+              ++checks;
+              if (!landed[t]) ++bad;
+            }
+        }
+      }
+    }
+  }
   std::printf("checks=%ld bad=%ld\n", checks, bad);
   return bad != 0 || checks == 0;
 }
