@@ -57,6 +57,9 @@ namespace cattn {
 #ifndef CATTN_DKDV_NB64  // dK/dV ring depth at D = 64 (unsplit)
 #define CATTN_DKDV_NB64 CATTN_BWD_NB64
 #endif
+#ifndef CATTN_DKDV_NB128  // dK/dV ring depth at D = 128
+#define CATTN_DKDV_NB128 CATTN_BWD_NB128
+#endif
 #ifndef CATTN_DKDV_GROUP  // iterations per barrier of the unsplit rings (where the ring is deep enough)
 #define CATTN_DKDV_GROUP 2
 #endif
@@ -765,7 +768,7 @@ template <int D> struct FwdCfg {
 };
 template <int D> struct BwdCfg {
   static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_BWD_NB128;
-  static constexpr int NB_DKDV = D == 64 ? CATTN_DKDV_NB64 : CATTN_BWD_NB128;
+  static constexpr int NB_DKDV = D == 64 ? CATTN_DKDV_NB64 : CATTN_DKDV_NB128;
 };
 
 template <int D, bool CAUSAL, int SPLIT, int NB>
