@@ -64,7 +64,7 @@ namespace cattn {
 #define CATTN_DKDV_GROUP 2
 #endif
 #ifndef CATTN_DQ_GROUP
-#define CATTN_DQ_GROUP 2
+#define CATTN_DQ_GROUP 3
 #endif
 #ifndef CATTN_FWD_GROUP
 #define CATTN_FWD_GROUP 2

@@ -61,10 +61,12 @@ constexpr int banded_rank(int bid, int n, int band) {
 // beyond it: this is their number.  Needs NB >= 2 G + need (the tiles a
 // group reads are then copied before its top).
 // Iterations per barrier a ring of NB slots can take with `split` parts and
-// `need` tiles of look-ahead: `want` when grouping is possible (one part, NB
-// a multiple of it, NB >= 2 want + need), else 1.
+// `need` tiles of look-ahead: the largest g <= want that groups the ring (one
+// part, NB a multiple of g, NB >= 2 g + need), else 1.
 constexpr int ring_group(int split, int NB, int need, int want) {
-  return (want > 1 && split == 1 && NB % want == 0 && NB >= 2 * want + need) ? want : 1;
+  for (int g = want; g > 1; --g)
+    if (split == 1 && NB % g == 0 && NB >= 2 * g + need) return g;
+  return 1;
 }
 constexpr int ring_group_in_flight(int i, int L, int NB, int G, int need) {
   const int last_issued = imin(L - 1, i + NB - G - 1);

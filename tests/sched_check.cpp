@@ -91,7 +91,9 @@ int main() {
     for (int G : {1, 2, 3, 4})
     for (int need : {0, 1}) {
       const int pro = NB - G;
-      if (NB % G || NB < 2 * G + need || ring_group(1, NB, need, G) != G) continue;
+      if (NB % G || NB < 2 * G + need) continue;
+      ++checks;
+      if (ring_group(1, NB, need, G) != G || ring_group(2, NB, need, G) != 1) ++bad;
       for (int L = 1; L <= 70; ++L) {
         std::vector<int> order;  // tiles in issue order
         for (int t = 0; t < pro && t < L; ++t) order.push_back(t);
