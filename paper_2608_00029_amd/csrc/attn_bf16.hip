@@ -536,16 +536,28 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 // diagonal, the ragged tile), and every wave issues the same copies per tile,
 // so that the common wait at the barrier is a compile-time count.
 // ---------------------------------------------------------------------------
+#ifndef CATTN_DKDV_BAND  // dK/dV work groups dealt in alternating directions per round (as the forward and dQ)
+#define CATTN_DKDV_BAND 1
+#endif
+#ifndef CATTN_DKDV_LEAN  // dK/dV at D = 64, unsplit: operands read where used, three waves per SIMD
+#define CATTN_DKDV_LEAN 1
+#endif
 template <int D, bool CAUSAL, int SPLIT, int NB>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
+constexpr bool dkdv_lean() {
+  return CATTN_DKDV_LEAN && D == 64 && SPLIT == 1;
+}
+template <int D, bool CAUSAL, int SPLIT, int NB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(dkdv_lean<D, CAUSAL, SPLIT, NB>() ? 3 : 1, 10)))
+void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
                                                                  const bf16* __restrict__ K,
                                                                  const bf16* __restrict__ V,
                                                                  const bf16* __restrict__ dO,
                                                                  const float* __restrict__ ws,
                                                                  bf16* __restrict__ dK, bf16* __restrict__ dV, int S,
-                                                                 int BH, int n_ktiles, float c, float scale, int H,
-                                                                 int seq_major) {
+                                                                 int BH, int n_ktiles, float c, float scale, int band,
+                                                                 int H, int seq_major) {
   typedef TileGeom<D> G;
+  constexpr bool LEAN = dkdv_lean<D, CAUSAL, SPLIT, NB>();
   constexpr int KG = 4 / SPLIT, BKV = 32 * KG;
   constexpr int TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
@@ -559,7 +571,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
   const int kg = w % KG, part = w / KG;
   int bh, kt;
-  tile_of_block(blockIdx.x, BH, n_ktiles, false, bh, kt);
+  tile_of_block_banded(blockIdx.x, BH, n_ktiles, false, CAUSAL ? band : 0, bh, kt);
   const Rows rw = rows_of(bh, H, S, D, seq_major);
   const int64_t base = rw.base;
   const int rs = rw.rs;
@@ -611,7 +623,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       }
     }
   };
-  constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
+  constexpr int NEED = LEAN ? 0 : 1;  // iteration i reads the tiles of iterations i .. i+NEED
   // With one part, the waves meet at a barrier every GROUP iterations: a wave
   // that runs late on its SIMD then holds the others back less often.
   constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_DKDV_GROUP);
@@ -644,16 +656,21 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
       const char* ldo = lq + TILE;
       const float* llse = (const float*)(lq + 2 * TILE);
       const float* ld = llse + 32;
-      if (i == i_lo) {  // a wave's first sub-block can be any tile: read it here
+      MB::frag dotr[2][DT], qtr[2][DT];
+      MB::frag qn[KS_D], don[KS_D];  // next tile of the part (on a wave's last tile: discarded)
+      if constexpr (LEAN) {
         read_rows<D>(lq, r, h, qf);
         read_rows<D>(ldo, r, h, dof);
+      } else {
+        if (i == i_lo) {  // a wave's first sub-block can be any tile: read it here
+          read_rows<D>(lq, r, h, qf);
+          read_rows<D>(ldo, r, h, dof);
+        }
+        read_trans<D>(ldo, lane, dotr);
+        read_trans<D>(lq, lane, qtr);
+        read_rows<D>(ring + sn * BUF, r, h, qn);
+        read_rows<D>(ring + sn * BUF + TILE, r, h, don);
       }
-      MB::frag dotr[2][DT], qtr[2][DT];
-      read_trans<D>(ldo, lane, dotr);
-      read_trans<D>(lq, lane, qtr);
-      MB::frag qn[KS_D], don[KS_D];  // next tile of the part (on a wave's last tile: discarded)
-      read_rows<D>(ring + sn * BUF, r, h, qn);
-      read_rows<D>(ring + sn * BUF + TILE, r, h, don);
       f32x16 s, dx;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -685,6 +702,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
         s[a] = p;
         dx[a] = -p * dx[a];  // dS = P (dP - D)
       }
+      if constexpr (LEAN) {
+        read_trans<D>(ldo, lane, dotr);
+        read_trans<D>(lq, lane, qtr);
+      }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const MB::frag pb = MB::pack(s, ks);
@@ -695,10 +716,12 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(const bf16* __r
           dkacc[dt] = MB::run(qtr[ks][dt], db, dkacc[dt]);
         }
       }
+      if constexpr (!LEAN) {
 #pragma unroll
-      for (int ks = 0; ks < KS_D; ++ks) {
-        qf[ks] = qn[ks];
-        dof[ks] = don[ks];
+        for (int ks = 0; ks < KS_D; ++ks) {
+          qf[ks] = qn[ks];
+          dof[ks] = don[ks];
+        }
       }
     });
   }
@@ -786,9 +809,14 @@ template <int D, bool CAUSAL, int SPLIT, int NB>
 static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
   constexpr int BKV = 128 / SPLIT;
   const int n_ktiles = (a.S + BKV - 1) / BKV;
+  // dealt in alternating directions only when every work group is resident
+  // from the start (three per CU)
+  const int band = CATTN_DKDV_BAND && dkdv_lean<D, CAUSAL, SPLIT, NB>() &&
+                           (int64_t)a.BH * n_ktiles <= 3 * (int64_t)cu_count() ? CATTN_BAND : 0;
   hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
-                     (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale, a.H, (int)a.seq_major);
+                     (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale,
+                     band, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 
