@@ -61,7 +61,7 @@ namespace cattn {
 #define CATTN_DKDV_NB128 CATTN_BWD_NB128
 #endif
 #ifndef CATTN_DKDV_GROUP  // iterations per barrier of the unsplit rings (where the ring is deep enough)
-#define CATTN_DKDV_GROUP 2
+#define CATTN_DKDV_GROUP 3
 #endif
 #ifndef CATTN_DQ_GROUP
 #define CATTN_DQ_GROUP 3
