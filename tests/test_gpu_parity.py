@@ -109,6 +109,32 @@ def test_workload_parity(cuda, w):
         assert torch.isfinite(t.float()).all()
 
 
+# Grids large enough for the unsplit D = 64 kernels (the three-wave dK/dV among
+# them), with ragged sequence ends and without the causal mask: the small cases
+# above all take the split (two-part) kernels.
+UNSPLIT = [
+    # B, H, S, causal
+    (4, 32, 1000, True),
+    (4, 32, 1000, False),
+    (2, 64, 993, True),
+    (4, 24, 1000, True),   # 768 work groups: resident all at once, banded order
+    (4, 32, 1024, False),
+]
+
+
+@pytest.mark.parametrize("case", UNSPLIT, ids=lambda c: "-".join(map(str, c)))
+def test_unsplit_grids_ragged_and_full(cuda, case):
+    B, H, S, causal = case
+    q, k, v, do = make_inputs(B, H, S, 64, "bf16", seed=9000 + S + B)
+    say(f"unsplit grid B={B} H={H} S={S} causal={causal}")
+    got = gpu_fwd_bwd(q, k, v, do, 0.125, causal)
+    heads = sampled_heads(B, H)
+    sel = lambda t: torch.stack([t[b, h] for b, h in heads])[None]  # noqa: E731
+    compare_all("bf16", tuple(sel(t) for t in got), *(sel(t) for t in (q, k, v, do)), 0.125, causal)
+    for t in got:
+        assert torch.isfinite(t.float()).all()
+
+
 def test_bwd_isolated_from_fwd(cuda):
     """GPU backward fed the oracle's O (rounded to the storage dtype) and LSE."""
     for dtype, S, D in (("f32", 128, 64), ("bf16", 512, 64), ("bf16", 256, 128)):
