@@ -79,6 +79,21 @@ def test_bshd_gpt2_small_full_size(cuda):
         assert torch.equal(g, r), f"{n}: [B,S,H,D] result differs from [B,H,S,D] at full size"
 
 
+@pytest.mark.parametrize("causal", [True, False])
+def test_bshd_unsplit_ragged_grid(cuda, causal):
+    """A grid that takes the unsplit D = 64 kernels, with a ragged sequence end,
+    in both storage orders: bit for bit the same results."""
+    B, H, S, D = 4, 32, 1000, 64
+    q, k, v, do = make_inputs(B, H, S, D, "bf16", seed=777 + int(causal))
+    say(f"layout bshd unsplit B{B} H{H} S{S} causal={causal}")
+    dev = [t.to(DEV) for t in (q, k, v, do)]
+    ref = run(*dev, 0.125, causal, "bhsd")
+    got = run(*[to_bshd(t) for t in dev], 0.125, causal, "bshd")
+    for n, g, r in zip(("o", "lse", "dq", "dk", "dv"), got, ref):
+        g = g if n == "lse" else to_bhsd(g)
+        assert torch.equal(g, r), f"{n}: [B,S,H,D] result differs from [B,H,S,D]"
+
+
 def test_layout_argument_checked(cuda):
     q = torch.zeros((1, 2, 64, 64), dtype=torch.bfloat16, device=DEV)
     with pytest.raises(ValueError):
