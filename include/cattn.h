@@ -42,7 +42,13 @@
  *    last tile is handled in the kernels); B * H * ceil(S / 128) < 2^31.
  *    B, H or S equal to 0 is an empty problem: the call returns CATTN_OK and
  *    touches no memory (pointers may then be NULL).
- *  - `scale` must be finite and > 0 (the softmax scale, e.g. 1/sqrt(D)).
+ *  - `scale` (the softmax scale, e.g. 1/sqrt(D)) must lie in [1e-20, 1e6]:
+ *    masked scores take the finite sentinel -1e30 (section 4.2), whose
+ *    base-2 exponential underflows to exactly 0 after scaling only for
+ *    scales well above 1e-28, and sentinel * scale must stay finite.
+ *  - Alignment: Q, K, V, O, dO, dQ, dK, dV and the backward workspace start
+ *    on a 16-byte boundary (the kernels move rows in 16-byte pieces); LSE on
+ *    a 4-byte boundary.  Any misaligned pointer is CATTN_ERR_INVALID_ARG.
  *  - `causal` != 0 selects the causal mask; 0 attends to every key.
  *
  * Errors: argument errors are detected on the host before anything is
@@ -61,8 +67,9 @@ extern "C" {
 
 typedef enum {
   CATTN_OK = 0,
-  CATTN_ERR_INVALID_ARG = 1,  /* NULL pointer, negative size, bad dtype, scale <= 0
-                                 or not finite, an output overlapping an input */
+  CATTN_ERR_INVALID_ARG = 1,  /* NULL or misaligned pointer, negative size, bad
+                                 dtype, scale outside [1e-20, 1e6] or not finite,
+                                 an output overlapping an input */
   CATTN_ERR_UNSUPPORTED = 2,  /* valid but not implemented: D not in {64, 128},
                                  S * D > 2^30, grid too large */
   CATTN_ERR_HIP = 3           /* the HIP runtime rejected a launch */
@@ -114,7 +121,7 @@ cattn_status cattn_attn_fwd(const void* q, const void* k, const void* v,
  *   dq,dk,dv : out, [B, H, S, D] `dtype` (must not overlap any input, each
  *              other, or the workspace)
  *   workspace: scratch of at least cattn_bwd_workspace_bytes(B, H, S, D)
- *              bytes, 4-byte aligned.  Its prior contents are ignored.  On
+ *              bytes, 16-byte aligned.  Its prior contents are ignored.  On
  *              return it holds, as float [B*H][2][Sp] with Sp = S rounded up
  *              to a multiple of 32: row 0 of head bh is D = rowsum(dO * O),
  *              row 1 is -LSE / scale; entries S..Sp-1 of both rows are 0.

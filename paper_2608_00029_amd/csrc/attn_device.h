@@ -50,8 +50,10 @@ constexpr float kLn2 = 0.69314718055994530942f;
 // Finite mask sentinel (section 4.2): masked scores get a large negative
 // finite value rather than -inf; the base-2 exponential maps it to exactly 0.
 constexpr float kMasked = -1.0e30f;
-// Largest base-2 exponent a probability may reach before the forward moves its
-// softmax offset (P <= 2^8 = 256, far inside float and bf16 range).
+// Largest base-2 exponent a probability may reach before the float32 forward
+// moves its softmax offset (P <= 2^8 = 256, far inside float range).  The bf16
+// forward uses a bound on the block's probability sum instead (2^32, see
+// kSumMax there).
 constexpr float kRescaleLog2 = 8.0f;
 
 // ---------------------------------------------------------------------------

@@ -18,6 +18,8 @@ namespace {
 
 thread_local char g_last_error[256] = "";
 
+constexpr float kMinScale = 1e-20f, kMaxScale = 1e6f;
+
 cattn_status fail(cattn_status st, const char* msg) {
   snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
   return st;
@@ -42,6 +44,11 @@ cattn_status check_shape(int B, int H, int S, int D, float scale, int dtype, boo
   if (D <= 0) return fail(CATTN_ERR_INVALID_ARG, "D must be positive");
   if (dtype != CATTN_F32 && dtype != CATTN_BF16) return fail(CATTN_ERR_INVALID_ARG, "dtype must be CATTN_F32 or CATTN_BF16");
   if (!(scale > 0.f) || !isfinite(scale)) return fail(CATTN_ERR_INVALID_ARG, "scale must be finite and > 0");
+  // Masked scores take a finite sentinel (-1e30) whose base-2 exponential must
+  // underflow to exactly 0 after the scale is applied, and sentinel * scale
+  // must stay finite: both hold with a wide margin inside this range.
+  if (scale < kMinScale || scale > kMaxScale)
+    return fail(CATTN_ERR_INVALID_ARG, "scale must lie in [1e-20, 1e6]");
   if (D != 64 && D != 128) return fail(CATTN_ERR_UNSUPPORTED, "head dimension D must be 64 or 128");
   if (B == 0 || H == 0 || S == 0) {
     *empty = true;
@@ -86,6 +93,10 @@ cattn_status cattn_attn_fwd_ex(const void* q, const void* k, const void* v, void
   cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
   if (st != CATTN_OK || empty) return st;
   if (!q || !k || !v || !o || !lse) return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
+  // the kernels move rows in 16-byte pieces
+  for (const void* p : {q, k, v, (const void*)o})
+    if (!aligned16(p)) return fail(CATTN_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+  if (((uintptr_t)lse & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "lse must be 4-byte aligned");
   const size_t esz = dtype == CATTN_BF16 ? 2 : 4;
   const size_t n = (size_t)B * H * S * D, nrow = (size_t)B * H * S;
   const Range rq = range_of(q, n * esz), rk = range_of(k, n * esz), rv = range_of(v, n * esz);
@@ -124,7 +135,11 @@ cattn_status bwd_common(const void* q, const void* k, const void* v, const void*
   if (!q || !k || !v || !dout || !lse || !workspace || (need_o && !o) || (need_dq && !dq) ||
       (need_dkdv && (!dk || !dv)))
     return fail(CATTN_ERR_INVALID_ARG, "NULL tensor pointer");
-  if (((uintptr_t)workspace & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "workspace must be 4-byte aligned");
+  // the kernels move rows (and workspace rows) in 16-byte pieces
+  for (const void* p : {q, k, v, dout, (const void*)workspace, need_o ? o : q, need_dq ? (const void*)dq : q,
+                        need_dkdv ? (const void*)dk : q, need_dkdv ? (const void*)dv : q})
+    if (!aligned16(p)) return fail(CATTN_ERR_INVALID_ARG, "tensors and the workspace must be 16-byte aligned");
+  if (((uintptr_t)lse & 3) != 0) return fail(CATTN_ERR_INVALID_ARG, "lse must be 4-byte aligned");
   const size_t esz = dtype == CATTN_BF16 ? 2 : 4;
   const size_t n = (size_t)B * H * S * D, nrow = (size_t)B * H * S;
   const size_t wsb = cattn_bwd_workspace_bytes(B, H, S, D);

@@ -65,6 +65,8 @@ P = [0x10000000 * (i + 1) for i in range(10)]
     ((1, 1, 16, 64, 0.0, 1, 1), b.CATTN_ERR_INVALID_ARG),     # scale must be > 0
     ((1, 1, 16, 64, float("nan"), 1, 1), b.CATTN_ERR_INVALID_ARG),
     ((1, 1, 16, 64, float("inf"), 1, 1), b.CATTN_ERR_INVALID_ARG),
+    ((1, 1, 16, 64, 1e-25, 1, 1), b.CATTN_ERR_INVALID_ARG),   # below the masked-sentinel range
+    ((1, 1, 16, 64, 1e7, 1, 1), b.CATTN_ERR_INVALID_ARG),     # above it
     ((1, 1, 16, 96, 0.125, 1, 1), b.CATTN_ERR_UNSUPPORTED),   # D not in {64, 128}
     ((1, 1, 16, 32, 0.125, 1, 0), b.CATTN_ERR_UNSUPPORTED),
     ((1, 1, 1 << 24, 128, 0.125, 1, 1), b.CATTN_ERR_UNSUPPORTED),  # S*D > 2^30
@@ -217,3 +219,33 @@ def test_memops_binding_refuses_cpu_tensors(lib):
         b.layernorm_fwd(x, torch.ones(8), torch.zeros(8))
     with pytest.raises(ValueError):
         b.sce_fwd(x)
+
+
+def test_fwd_rejects_misaligned_pointers(lib):
+    """Q, K, V, O must start on 16 bytes (rows move in 16-byte pieces), LSE on 4."""
+    B, H, S, D = 1, 2, 64, 64
+    good = [P[0], P[1], P[2], P[3], P[4]]  # never passed as is: that call would launch
+    for i, off in ((0, 2), (1, 8), (2, 4), (3, 2), (4, 2)):
+        a = list(good)
+        a[i] += off
+        assert b.raw_fwd(*a, B, H, S, D, 0.125, 1, 1) == b.CATTN_ERR_INVALID_ARG, (i, off)
+        assert "aligned" in b.last_error_string()
+
+
+def test_bwd_rejects_misaligned_pointers(lib):
+    B, H, S, D = 1, 2, 64, 64
+    names = ("q", "k", "v", "o", "do", "lse", "dq", "dk", "dv", "ws")
+    for i, name in enumerate(names):
+        a = list(P)
+        a[i] += 2 if name == "lse" else 8
+        assert b.raw_bwd(*a, B, H, S, D, 0.125, 1, 1) == b.CATTN_ERR_INVALID_ARG, name
+        assert "aligned" in b.last_error_string(), name
+
+
+def test_scale_range_boundaries_accepted(lib):
+    """The ends of the supported scale range pass the argument checks (the call
+    then fails only on its NULL pointers)."""
+    for scale in (1e-20, 1e6):
+        assert b.raw_fwd(0, 0, 0, 0, 0, 1, 1, 16, 64, scale, 1, 1) == b.CATTN_ERR_INVALID_ARG
+        assert "NULL" in b.last_error_string()
+
