@@ -185,3 +185,55 @@ def attn_probabilities(q, k, scale: float, causal: bool = True):
             s = masked_scores(q[bi, hi], k[bi, hi], scale, causal)
             out[bi, hi] = probabilities(s, row_logsumexp(s))
     return out
+
+
+def head_term_magnitudes(q, k, v, do, scale, causal):
+    """Sizes of the terms each output element of one (batch, head) sums, for
+    error bounds in tests (float64; q, k, v, do: [S, D]).
+
+    Every output of section 4.2's forward and backward is a contraction whose
+    terms are products of a softmax-derived factor and an input row:
+    O_i = sum_j P_ij V_j, dV_j = sum_i P_ij dO_i, dQ_i = scale sum_j dS_ij K_j,
+    dK_j = scale sum_i dS_ij Q_i.  A rounding of relative size u in each term
+    (P or dS rounded to bf16, a float sum of n terms) moves an output element
+    by at most u times the sum of its terms' absolute values, which is what
+    this returns:
+
+        m_o  = P |V|           m_dv = P^T |dO|
+        g_dq = |dS| |K|        g_dk = |dS|^T |Q|
+
+    D = rowsum(dO * O) enters every dS_ij of row i through P_ij; an error in O
+    of at most t * m_o moves D_i by at most t * a_i, a_i = sum_d |dO_id| m_o_id,
+    and therefore dQ and dK by at most t times
+
+        h_dq = (a * P) |K|     h_dk = (a * P)^T |Q|     (a scales row i of P).
+
+    Returns a dict of these arrays ([S, D] each; a: [S]).
+    """
+    s = masked_scores(q, k, scale, causal)
+    p = probabilities(s, row_logsumexp(s))
+    o = p @ v
+    dp = do @ v.T
+    d = np.sum(do * o, axis=1)
+    ads = np.abs(p * (dp - d[:, None]))
+    m_o = p @ np.abs(v)
+    a = np.sum(np.abs(do) * m_o, axis=1)
+    ap = a[:, None] * p
+    return {"m_o": m_o, "m_dv": p.T @ np.abs(do), "g_dq": ads @ np.abs(k), "g_dk": ads.T @ np.abs(q),
+            "a": a, "h_dq": ap @ np.abs(k), "h_dk": ap.T @ np.abs(q)}
+
+
+def attn_term_magnitudes(q, k, v, do, scale: float, causal: bool = True):
+    """head_term_magnitudes for every (batch, head) of [B, H, S, D] inputs:
+    a dict of [B, H, S, D] arrays (a: [B, H, S])."""
+    q, k, v, do = _as_f64(q), _as_f64(k), _as_f64(v), _as_f64(do)
+    b, h, n, d = q.shape
+    out = None
+    for bi in range(b):
+        for hi in range(h):
+            m = head_term_magnitudes(q[bi, hi], k[bi, hi], v[bi, hi], do[bi, hi], scale, causal)
+            if out is None:
+                out = {key: np.empty((b, h) + val.shape) for key, val in m.items()}
+            for key, val in m.items():
+                out[key][bi, hi] = val
+    return out

@@ -3,9 +3,12 @@
 Small cases compare every output element; they span several 128-row query
 tiles, 64-row key tiles and a ragged last tile, in both dtypes, both head
 dimensions, causal and not.  The five named workloads run at full size in the
-launch configuration the benchmark times and are compared on whole sampled
-(batch, head) slices, which the oracle computes exactly.  The backward is
-end-to-end: it consumes the GPU forward's O and LSE.
+launch configuration the benchmark times: the GPT-2 shapes are compared on
+every (batch, head), the long-context one and the larger sweep shapes on eight
+(batch, head) slices (the first and last head of the first and last batch
+among them).  The backward is end-to-end: it consumes the GPU forward's O and
+LSE.  bf16 results meet the global tolerances and, element by element and row
+by row, the per-element bound derived in parity_util.
 """
 
 import math
@@ -17,7 +20,7 @@ import torch
 import oracle.attn_oracle as orc
 from paper_2608_00029_amd import attn_bwd, attn_fwd
 from paper_2608_00029_amd.workloads import SWEEP, WORKLOADS, make_inputs, workload_inputs
-from parity_util import check_tensor, say, to64
+from parity_util import bf16_bounds, check_bounded, check_tensor, max_abs, say, to64
 
 pytestmark = pytest.mark.gpu
 
@@ -36,9 +39,26 @@ def compare_all(dtype, got, q, k, v, do, scale, causal):
     o, lse, dq, dk, dv = got
     ro, rlse = orc.attn_fwd(q, k, v, scale, causal)
     rdq, rdk, rdv = orc.attn_bwd(q, k, v, do, scale, causal)
-    rep = [check_tensor(n, dtype, g, r) for n, g, r in
-           (("o", o, ro), ("lse", lse, rlse), ("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv))]
+    pairs = (("o", o, ro), ("lse", lse, rlse), ("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv))
+    rep = [check_tensor(n, dtype, g, r) for n, g, r in pairs]
+    if dtype == "bf16":
+        bounds = bf16_bounds(q, k, orc.attn_term_magnitudes(q, k, v, do, scale, causal), scale, max_abs(lse, rlse))
+        rep += [check_bounded(n, g, r, bounds[n]) for n, g, r in pairs if n != "lse"]
     print("  " + "  ".join(rep), flush=True)
+
+
+def parity_heads(B, H, S):
+    """Every (batch, head) when the oracle's work stays near the GPT-2 shapes';
+    otherwise eight, including the first and last head of the first and last batch."""
+    if B * H * S * S <= 128 * 1024 * 1024:
+        return [(b, h) for b in range(B) for h in range(H)]
+    cand = [(0, 0), (0, H - 1), (B - 1, 0), (B - 1, H - 1), (B // 2, H // 2), (0, H // 2), (B - 1, H // 2),
+            (B // 2, 0), (0, H // 4), (B - 1, 3 * H // 4), (0, 3 * H // 4), (B - 1, H // 4)]
+    out = []
+    for c in cand:
+        if c not in out:
+            out.append(c)
+    return sorted(out[:8])
 
 
 SMALL = [
@@ -91,17 +111,14 @@ def test_empty_problem(cuda):
         assert o.shape == shape and dq.shape == shape and lse.shape == shape[:3]
 
 
-def sampled_heads(B, H):
-    return sorted({(0, 0), (B // 2, H // 2), (B - 1, H - 1)})
-
-
 @pytest.mark.parametrize("w", WORKLOADS + SWEEP, ids=lambda w: w.name)
 def test_workload_parity(cuda, w):
-    """Full-size run; every element of the sampled (batch, head) slices is compared."""
+    """Full-size run; every element of the compared (batch, head) slices is checked."""
     q, k, v, do = workload_inputs(w)
     say(f"workload {w.name}")
     got = gpu_fwd_bwd(q, k, v, do, w.scale, w.causal)
-    heads = sampled_heads(w.B, w.H) if w.B * w.H > 4 else [(b, h) for b in range(w.B) for h in range(w.H)]
+    heads = parity_heads(w.B, w.H, w.S)
+    print(f"  comparing {len(heads)} of {w.B * w.H} (batch, head) slices", flush=True)
     sel = lambda t: torch.stack([t[b, h] for b, h in heads])[None]  # noqa: E731
     qs, ks, vs, dos = (sel(t) for t in (q, k, v, do))
     compare_all(w.dtype, tuple(sel(t) for t in got), qs, ks, vs, dos, w.scale, w.causal)
@@ -128,7 +145,7 @@ def test_unsplit_grids_ragged_and_full(cuda, case):
     q, k, v, do = make_inputs(B, H, S, 64, "bf16", seed=9000 + S + B)
     say(f"unsplit grid B={B} H={H} S={S} causal={causal}")
     got = gpu_fwd_bwd(q, k, v, do, 0.125, causal)
-    heads = sampled_heads(B, H)
+    heads = parity_heads(B, H, S)
     sel = lambda t: torch.stack([t[b, h] for b, h in heads])[None]  # noqa: E731
     compare_all("bf16", tuple(sel(t) for t in got), *(sel(t) for t in (q, k, v, do)), 0.125, causal)
     for t in got:
@@ -150,6 +167,11 @@ def test_bwd_isolated_from_fwd(cuda):
         rdq, rdk, rdv = orc.attn_bwd(q, k, v, do, scale, True)
         for n, g, r in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
             check_tensor(n, dtype, g.cpu(), r)
+        if dtype == "bf16":
+            bounds = bf16_bounds(q, k, orc.attn_term_magnitudes(q, k, v, do, scale, True), scale,
+                                 max_abs(lse.cpu(), rlse))
+            for n, g, r in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
+                check_bounded(n, g.cpu(), r, bounds[n])
 
 
 def test_gpu_invariants(cuda):

@@ -319,3 +319,44 @@ def test_planted_mistake_is_caught(name):
             except (AssertionError, ValueError, FloatingPointError):
                 caught.append(check.__name__)
     assert caught, f"mutant {name} passed every check"
+
+
+# --------------------------------------------------------------------------------------
+# The term magnitudes the GPU parity tests derive their per-element error bounds from.
+# --------------------------------------------------------------------------------------
+
+def test_term_magnitudes_hand_worked():
+    """Every magnitude of the S=3 hand-worked example (derived by hand, golden file)."""
+    g = json.load(open(GOLDEN))
+    inp = g["inputs"]
+    q, k, v, do = (_vec(inp[n]).reshape(1, 1, 3, 1) for n in ("q", "k", "v", "do"))
+    m = orc.attn_term_magnitudes(q, k, v, do, inp["scale"], True)
+    for name, exp in g["causal_magnitudes"].items():
+        np.testing.assert_allclose(m[name].reshape(-1), _vec(exp), rtol=0, atol=1e-13, err_msg=name)
+
+
+def test_term_magnitudes_bound_the_outputs():
+    """Triangle inequality: each output element is at most its terms' absolute sum,
+    with equality when every term is nonnegative (V >= 0 for O, dO >= 0 for dV)."""
+    q, k, v, do = (_rand((2, 2, 37, 8), s, 2.0) for s in range(90, 94))
+    for causal in (True, False):
+        m = orc.attn_term_magnitudes(q, k, v, do, 0.3, causal)
+        o, _ = orc.attn_fwd(q, k, v, 0.3, causal)
+        dq, dk, dv = orc.attn_bwd(q, k, v, do, 0.3, causal)
+        tol = 1e-12
+        assert np.all(np.abs(o) <= m["m_o"] * (1 + tol) + tol)
+        assert np.all(np.abs(dv) <= m["m_dv"] * (1 + tol) + tol)
+        assert np.all(np.abs(dq) <= 0.3 * m["g_dq"] * (1 + tol) + tol)
+        assert np.all(np.abs(dk) <= 0.3 * m["g_dk"] * (1 + tol) + tol)
+        # a_i bounds |D_i| = |rowsum(dO * O)|
+        d = np.sum(do * o, axis=-1)
+        assert np.all(np.abs(d) <= m["a"] * (1 + tol) + tol)
+        vp, dop = np.abs(v), np.abs(do)
+        mp = orc.attn_term_magnitudes(q, k, vp, dop, 0.3, causal)
+        op, _ = orc.attn_fwd(q, k, vp, 0.3, causal)
+        _, _, dvp = orc.attn_bwd(q, k, vp, dop, 0.3, causal)
+        np.testing.assert_allclose(mp["m_o"], op, rtol=1e-13, atol=0)
+        np.testing.assert_allclose(mp["m_dv"], dvp, rtol=1e-13, atol=0)
+        # h = (a * P)|X|: with a = 1 it is P|X|, which for X >= 0 is the forward itself
+        np.testing.assert_allclose(mp["h_dq"] / mp["a"][..., None],
+                                   orc.attn_fwd(q, k, np.abs(k), 0.3, causal)[0], rtol=1e-12, atol=0)
