@@ -587,21 +587,27 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
 
   const int k0 = kt * BKV, kw = k0 + 32 * kg, my_k = kw + r;
   // 32-query tiles of the workgroup: from the one holding k0 (causal: the loop's
-  // lower bound is raised to the diagonal) to the end of the sequence.
+  // lower bound is raised to the diagonal) to the end of the sequence, walked
+  // from the LAST tile down (walk position t holds query tile nt - 1 - t).  The
+  // work groups of one head then start on the same tile and stream the same
+  // Q/dO tiles at about the same time, so that one HBM fetch of a tile serves
+  // all of them from L2; the masked diagonal tile comes last.
+  const int nt = (S + 31) / 32;                 // query tiles of the sequence
   const int jt0 = CAUSAL ? k0 / 32 : 0;
-  const int n = (S + 31) / 32 - jt0;
-  const int L = (n + SPLIT - 1) / SPLIT;        // iterations; part p owns tiles [p*L, min(n, p*L + L))
+  const int n = nt - jt0;
+  const int L = (n + SPLIT - 1) / SPLIT;        // iterations; part p owns walk positions [p*L, min(n, p*L + L))
   const int n_last = n - (SPLIT - 1) * L;       // tiles of the last part (<= L)
-  const int jb = CAUSAL ? kw / 32 : 0;          // this wave's first sub-block
-  const int je = kw >= S ? jb : (S + 31) / 32;  // ... and one past its last
-  const int tb = part * L;                      // this wave's part starts at tile tb
-  // iteration indices, relative to this wave's part
-  const int i_lo = max(0, jb - jt0 - tb);                                         // first active
-  const int i_span = max(0, min(part == SPLIT - 1 ? n_last : L, je - jt0 - tb) - i_lo);  // active count
-  const int i_diag = CAUSAL ? jb - jt0 - tb : -1;                                 // causal diagonal
-  const int t_rag = (S % 32) ? (S - 1) / 32 - jt0 : -1;                           // ragged tile (workgroup index)
-  const int i_rag = t_rag - tb;                                                   // ... in this part
-  // copies: iteration x of the ring holds tile p*L + x of every part p with x < L (x < n_last for the last)
+  const int jb = CAUSAL ? kw / 32 : 0;          // this wave's first query tile
+  const int je = kw >= S ? jb : nt;             // ... and one past its last
+  const int tb = part * L;                      // this wave's part starts at walk position tb
+  // iteration indices, relative to this wave's part: the wave's tiles jb .. je-1
+  // sit at walk positions nt - je .. nt - 1 - jb
+  const int i_lo = max(0, nt - je - tb);                                             // first active
+  const int i_span = max(0, min(part == SPLIT - 1 ? n_last : L, nt - jb - tb) - i_lo);  // active count
+  const int i_diag = CAUSAL ? nt - 1 - jb - tb : -1;                                 // causal diagonal
+  const int t_rag = (S % 32) ? 0 : -1;           // walk position of the ragged (last) tile
+  const int i_rag = t_rag - tb;                  // ... in this part
+  // copies: iteration x of the ring holds walk position p*L + x of every part p with x < L (x < n_last for the last)
 
   TileCopy<D> tc;
   tc.init(w, lane, rs);
@@ -610,7 +616,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
     for (int p = 0; p < SPLIT; ++p) {
       if (p < SPLIT - 1 || x < n_last) {
         const int t = p * L + x;
-        const int row0 = (jt0 + t) * 32;
+        const int row0 = (nt - 1 - t) * 32;
         char* b = smem + (p * NB + decltype(slc)::value) * BUF;
         if (t != t_rag) {
           tc.copy_full(Qb, row0, b);
@@ -662,7 +668,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
         read_rows<D>(lq, r, h, qf);
         read_rows<D>(ldo, r, h, dof);
       } else {
-        if (i == i_lo) {  // a wave's first sub-block can be any tile: read it here
+        if (i == i_lo) {  // a wave's first sub-block: read it here
           read_rows<D>(lq, r, h, qf);
           read_rows<D>(ldo, r, h, dof);
         }
@@ -689,7 +695,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
       }
       // s[a], dx[a]: S - LSE/scale and D - dP of query 32j + acc_row(a, h), key my_k
       if (i == i_diag || i == i_rag) {  // the causal diagonal or the ragged end of the sequence
-        const int qs = (jt0 + tb + i) * 32;
+        const int qs = (nt - 1 - tb - i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int qry = qs + acc_row(a, h);
