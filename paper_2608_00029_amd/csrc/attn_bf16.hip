@@ -73,6 +73,18 @@ namespace cattn {
 #define CATTN_DKDV_NB64S 4
 #endif
 
+// Causal loop clamping (section 4.2): the loops visit only the tiles that hold
+// visible (query, key) pairs -- the forward and dQ loops stop at the diagonal,
+// the dK/dV loop starts there.  A test build (CATTN_TEST_NOCLAMP=1, never the
+// product library) visits every tile instead, masking the ones past the
+// diagonal entirely, to show that clamping changes no result: a fully masked
+// tile has P = exp2(-1e30 c - m c) = 0 exactly, adds 0 to every sum and never
+// moves the softmax offset.
+#ifndef CATTN_TEST_NOCLAMP
+#define CATTN_TEST_NOCLAMP 0
+#endif
+constexpr bool kNoClamp = CATTN_TEST_NOCLAMP != 0;
+
 // The forward keeps a softmax offset that moves only when a block's partial
 // probability sum exceeds this bound (or is not finite).  Probabilities are
 // then at most 2^32 (offset at most 32 below the running max, base 2), far
@@ -124,10 +136,10 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const bf16* Vb = V + base;
 
   const int q0 = qt * BQ, qw = q0 + 32 * qg, my_q = qw + r;
-  const int kend = CAUSAL ? min(S, q0 + BQ) : S;   // causal loop clamping (workgroup)
+  const int kend = CAUSAL && !kNoClamp ? min(S, q0 + BQ) : S;   // causal loop clamping (workgroup)
   const int n = (kend + 31) / 32;                   // 32-key tiles of the workgroup
   const int L = (n + SPLIT - 1) / SPLIT;            // tiles per part (the last may be short)
-  const int kend_w = qw >= S ? 0 : (CAUSAL ? min(S, qw + 32) : S);
+  const int kend_w = qw >= S ? 0 : (CAUSAL && !kNoClamp ? min(S, qw + 32) : S);
   const int nsb = (kend_w + 31) / 32;               // tiles this wave's queries need
   const int tb = part * L;                          // this wave's tiles: [tb, te)
   const int te = min(nsb, min(n, tb + L));
@@ -138,7 +150,9 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   const int t_rag = (S % 32) && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
   // the iteration (in this wave's part) whose tile must be masked: the wave's
   // last tile when it straddles the causal diagonal or the end of the sequence
-  const int i_mask = nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
+  // (without the clamp, every tile from the one holding the diagonal on: i >= i_mask)
+  const int i_mask = CAUSAL && kNoClamp ? qw / 32 - tb
+                     : nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
 
   TileCopy<D> tc;
   tc.init(w, lane, rs);
@@ -215,7 +229,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
       f32x16& sa_ = sa[pc];
       // causal diagonal / ragged end: only the last tile of the wave's queries
-      if (i == i_mask) {
+      if (CAUSAL && kNoClamp ? i >= i_mask : i == i_mask) {
         const int k0 = (tb + i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
@@ -373,10 +387,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int Sp = ws_rows(S);
 
   const int q0 = qt * BQ, qw = q0 + 32 * qg, my_q = qw + r;
-  const int kend = CAUSAL ? min(S, q0 + BQ) : S;
+  const int kend = CAUSAL && !kNoClamp ? min(S, q0 + BQ) : S;
   const int n = (kend + 31) / 32;          // 32-key tiles of the workgroup
   const int L = (n + SPLIT - 1) / SPLIT;   // tiles per part (the last may be short)
-  const int kend_w = qw >= S ? 0 : (CAUSAL ? min(S, qw + 32) : S);
+  const int kend_w = qw >= S ? 0 : (CAUSAL && !kNoClamp ? min(S, qw + 32) : S);
   const int nsb = (kend_w + 31) / 32;      // tiles this wave's queries need
   const int tb = part * L;                 // this wave's tiles: [tb, te)
   const int te = min(nsb, min(n, tb + L));
@@ -387,7 +401,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
   const int t_rag = (S % 32) && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
   // the iteration (in this wave's part) whose tile must be masked: the wave's
   // last tile when it straddles the causal diagonal or the end of the sequence
-  const int i_mask = nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
+  // (without the clamp, every tile from the one holding the diagonal on: i >= i_mask)
+  const int i_mask = CAUSAL && kNoClamp ? qw / 32 - tb
+                     : nsb > 0 && ((CAUSAL && (nsb - 1) * 32 + 31 > qw) || nsb * 32 > S) ? nsb - 1 - tb : -1;
 
   TileCopy<D> tc;
   tc.init(w, lane, rs);
@@ -464,7 +480,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
         s = MB::run(kf[ks], qf[ks], s);
         dx = MB::run(vfr[ks], dof[ks], dx);  // D - dP^T
       }
-      if (i == i_mask) {
+      if (CAUSAL && kNoClamp ? i >= i_mask : i == i_mask) {
         const int k0 = j * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
@@ -593,18 +609,19 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
   // Q/dO tiles at about the same time, so that one HBM fetch of a tile serves
   // all of them from L2; the masked diagonal tile comes last.
   const int nt = (S + 31) / 32;                 // query tiles of the sequence
-  const int jt0 = CAUSAL ? k0 / 32 : 0;
+  const int jt0 = CAUSAL && !kNoClamp ? k0 / 32 : 0;
   const int n = nt - jt0;
   const int L = (n + SPLIT - 1) / SPLIT;        // iterations; part p owns walk positions [p*L, min(n, p*L + L))
   const int n_last = n - (SPLIT - 1) * L;       // tiles of the last part (<= L)
-  const int jb = CAUSAL ? kw / 32 : 0;          // this wave's first query tile
+  const int jb = CAUSAL && !kNoClamp ? kw / 32 : 0;  // this wave's first query tile
   const int je = kw >= S ? jb : nt;             // ... and one past its last
   const int tb = part * L;                      // this wave's part starts at walk position tb
   // iteration indices, relative to this wave's part: the wave's tiles jb .. je-1
   // sit at walk positions nt - je .. nt - 1 - jb
   const int i_lo = max(0, nt - je - tb);                                             // first active
   const int i_span = max(0, min(part == SPLIT - 1 ? n_last : L, nt - jb - tb) - i_lo);  // active count
-  const int i_diag = CAUSAL ? nt - 1 - jb - tb : -1;                                 // causal diagonal
+  // causal diagonal (without the clamp, the tiles before it come after it in the walk: i >= i_diag)
+  const int i_diag = CAUSAL ? nt - 1 - kw / 32 - tb : -1;
   const int t_rag = (S % 32) ? 0 : -1;           // walk position of the ragged (last) tile
   const int i_rag = t_rag - tb;                  // ... in this part
   // copies: iteration x of the ring holds walk position p*L + x of every part p with x < L (x < n_last for the last)
@@ -694,7 +711,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
         dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
       }
       // s[a], dx[a]: S - LSE/scale and D - dP of query 32j + acc_row(a, h), key my_k
-      if (i == i_diag || i == i_rag) {  // the causal diagonal or the ragged end of the sequence
+      if ((CAUSAL && kNoClamp ? i >= i_diag : i == i_diag) || i == i_rag) {  // the causal diagonal or the ragged end
         const int qs = (nt - 1 - tb - i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
@@ -841,8 +858,11 @@ static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
   if constexpr (D == 64) {
     // Split each query tile's key range over two parts when the unsplit grid
     // (128-query tiles) cannot fill the GPU's workgroup slots (three per CU).
-    const bool split = CATTN_FWD_SPLIT_MODE == 1 ||
-                       (CATTN_FWD_SPLIT_MODE == 0 && (int64_t)a.BH * ((a.S + 127) / 128) < 3 * (int64_t)cu_count());
+    // (The no-clamp test build never splits: a split part would then start on
+    // tiles that are fully masked for its queries, with no real score to set
+    // the softmax offset from.)
+    const bool split = !kNoClamp && (CATTN_FWD_SPLIT_MODE == 1 ||
+                       (CATTN_FWD_SPLIT_MODE == 0 && (int64_t)a.BH * ((a.S + 127) / 128) < 3 * (int64_t)cu_count()));
     if (split) return launch_fwd_split<D, CAUSAL, 2, FwdCfg<D>::NB_SPLIT>(a, st);
   }
   return launch_fwd_split<D, CAUSAL, 1, FwdCfg<D>::NB>(a, st);
@@ -863,7 +883,8 @@ static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   // then sets the time.  With a full grid the unsplit kernels have less
   // overhead per unit of work.
   bool split = false;
-  if constexpr (D == 64) split = (int64_t)a.BH * ((a.S + 127) / 128) < CATTN_BWD_SPLIT_WG_PER_CU * (int64_t)cu_count();
+  if constexpr (D == 64)
+    split = !kNoClamp && (int64_t)a.BH * ((a.S + 127) / 128) < CATTN_BWD_SPLIT_WG_PER_CU * (int64_t)cu_count();
   if (phase != 2) {
     hipError_t e;
     if constexpr (D == 64) {
