@@ -178,6 +178,32 @@ cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v,
                                  float scale, int causal, int dtype, void* stream);
 
 /*
+ * cattn_attn_bwd_ex without the workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The workspace is a fixed 8 MiB array in
+ * the library's device memory instead, one per GPU, held until the process
+ * ends; this call allocates nothing (no hipMalloc, no allocating library
+ * routine).  Results are bit for bit those of cattn_attn_bwd_ex.
+ *
+ *   Limit: 2 * B * H * Sp * 4 <= 8 MiB, Sp = S rounded up to a multiple of 32
+ *   (e.g. B*H*Sp <= 2^20: GPT-2 small B8 H12 S1024 uses 3 MiB); larger
+ *   problems return CATTN_ERR_UNSUPPORTED before anything is enqueued.
+ *   Sharing: every call on one GPU uses that GPU's one array.  The backward
+ *   writes all of the part it reads before reading it, so nothing needs to
+ *   be cleared between calls, but calls that overlap in time on one GPU (on
+ *   different streams or threads) race on the array: order them.  The first
+ *   call on a device looks up the array's device address (a HIP runtime
+ *   query, no allocation).
+ *   Everything else -- arguments, layouts, error behaviour -- as for
+ *   cattn_attn_bwd_ex.
+ */
+cattn_status cattn_attn_bwd_noalloc(const void* q, const void* k, const void* v,
+                                    const void* o, const void* dout, const float* lse,
+                                    void* dq, void* dk, void* dv,
+                                    int B, int H, int S, int D,
+                                    float scale, int causal, int dtype, int layout, void* stream);
+
+/*
  * Fused language-model loss head, forward (section 4.1, case study "Fusing a
  * Reduction into a Contraction Epilogue"; the fused loss-head evaluation).
  * For hidden states X, the head's weight W (no bias) and target ids y:

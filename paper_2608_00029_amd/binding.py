@@ -28,7 +28,7 @@ EXPORTED = ("cattn_attn_fwd", "cattn_attn_bwd", "cattn_attn_fwd_ex", "cattn_attn
             "cattn_attn_bwd_dkdv", "cattn_lmhead_fwd", "cattn_lmhead_workspace_bytes",
             "cattn_bwd_workspace_bytes", "cattn_status_string", "cattn_last_error_string",
             "cattn_layernorm_fwd", "cattn_layernorm_bwd", "cattn_layernorm_bwd_workspace_bytes", "cattn_gelu_fwd",
-            "cattn_gelu_bwd", "cattn_sce_fwd", "cattn_sce_bwd")
+            "cattn_gelu_bwd", "cattn_sce_fwd", "cattn_sce_bwd", "cattn_attn_bwd_noalloc")
 
 
 class CattnError(RuntimeError):
@@ -58,6 +58,8 @@ def lib() -> ctypes.CDLL:
         L.cattn_attn_fwd_ex.restype = i
         L.cattn_attn_bwd_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, i, vp]
         L.cattn_attn_bwd_ex.restype = i
+        L.cattn_attn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, i, vp]
+        L.cattn_attn_bwd_noalloc.restype = i
         L.cattn_attn_bwd_dq.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
         L.cattn_attn_bwd_dq.restype = i
         L.cattn_attn_bwd_dkdv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
@@ -199,6 +201,23 @@ def attn_bwd(q, k, v, o, do, lse, scale: float, causal: bool = True, dq=None, dk
                                  _dtype_code(q), _LAYOUTS[layout], _stream(q.device))
     if st != CATTN_OK:
         raise CattnError(st, "cattn_attn_bwd_ex", last_error_string())
+    return dq, dk, dv
+
+
+def attn_bwd_noalloc(q, k, v, o, do, lse, dq, dk, dv, scale: float, causal: bool = True, layout: str = "bhsd"):
+    """attn_bwd into caller-provided dq, dk, dv through cattn_attn_bwd_noalloc:
+    nothing is allocated (the workspace is the library's static device array)."""
+    B, H, S, D = _shape(q, layout)
+    if q.device.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do), ("dq", dq), ("dk", dk), ("dv", dv)):
+        _check(n, t, q.shape, q.dtype, q.device)
+    _check("lse", lse, (B, H, S), torch.float32, q.device)
+    st = lib().cattn_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq), _ptr(dk),
+                                      _ptr(dv), B, H, S, D, float(scale), int(bool(causal)), _dtype_code(q),
+                                      _LAYOUTS[layout], _stream(q.device))
+    if st != CATTN_OK:
+        raise CattnError(st, "cattn_attn_bwd_noalloc", last_error_string())
     return dq, dk, dv
 
 

@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/cattn.h"
 #include "attn_launch.h"
 #include "lmhead_launch.h"
@@ -201,6 +203,67 @@ cattn_status cattn_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
                                  float scale, int causal, int dtype, void* stream) {
   return bwd_common(q, k, v, nullptr, dout, lse, nullptr, dk, dv, const_cast<float*>(workspace), B, H, S, D,
                     scale, causal, dtype, CATTN_BHSD, stream, 2);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Backward workspace of cattn_attn_bwd_noalloc: a fixed device array, one copy
+// per GPU the library runs on, held until the process ends.  Host code never
+// uses the array's name as an address: the device address of each GPU's copy
+// comes from hipGetSymbolAddress, looked up once per device with that device
+// current, and is what the kernels receive.
+constexpr size_t kNoAllocWsBytes = size_t(8) << 20;
+__device__ __align__(256) float scratch[kNoAllocWsBytes / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, or NULL after writing the error.
+float* scratch_on_current_device(cattn_status* st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *st = hip_status(e);
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    *st = fail(CATTN_ERR_UNSUPPORTED, "device index beyond the static scratch table");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      *st = e != hipSuccess ? hip_status(e) : fail(CATTN_ERR_HIP, "no device address for the static scratch");
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+cattn_status cattn_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                                    const float* lse, void* dq, void* dk, void* dv, int B, int H, int S, int D,
+                                    float scale, int causal, int dtype, int layout, void* stream) {
+  g_last_error[0] = '\0';
+  bool empty;
+  cattn_status st = check_shape(B, H, S, D, scale, dtype, &empty);
+  if (st != CATTN_OK || empty) return st;
+  if (cattn_bwd_workspace_bytes(B, H, S, D) > kNoAllocWsBytes)
+    return fail(CATTN_ERR_UNSUPPORTED, "the backward workspace this shape needs exceeds the 8 MiB static scratch "
+                                       "(2 * B * H * ceil(S / 32) * 32 floats)");
+  st = CATTN_OK;
+  float* ws = scratch_on_current_device(&st);
+  if (!ws) return st;
+  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, ws, B, H, S, D, scale, causal, dtype, layout, stream, 0);
 }
 
 size_t cattn_lmhead_workspace_bytes(int M, int N, int K) {

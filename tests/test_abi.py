@@ -249,3 +249,13 @@ def test_scale_range_boundaries_accepted(lib):
         assert b.raw_fwd(0, 0, 0, 0, 0, 1, 1, 16, 64, scale, 1, 1) == b.CATTN_ERR_INVALID_ARG
         assert "NULL" in b.last_error_string()
 
+
+def test_noalloc_rejects_shapes_beyond_its_static_scratch(lib):
+    """8 MiB of static workspace holds 2 * B * H * Sp floats up to 2^21; larger
+    shapes are refused on the host before any HIP call."""
+    vp = ctypes.c_void_p
+    args = [vp(p) for p in P[:9]]
+    st = lib.cattn_attn_bwd_noalloc(*args, 16, 32, 4096, 64, ctypes.c_float(0.125), 1, 1, 0, vp(0))
+    assert st == b.CATTN_ERR_UNSUPPORTED
+    assert "static scratch" in b.last_error_string()
+    assert b.workspace_bytes(16, 32, 4096, 64) > 8 << 20 >= b.workspace_bytes(16, 32, 2048, 64)
