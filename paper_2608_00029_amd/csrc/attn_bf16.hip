@@ -111,7 +111,7 @@ constexpr float kSumMax = 4294967296.0f;
 // computes the block max, moves m, rescales O and the running sum, and redoes
 // the block.  No per-block max is computed on the common path.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL, int SPLIT, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                             const bf16* __restrict__ V, bf16* __restrict__ O,
                                                             float* __restrict__ LSE, int S, int BH, int n_qtiles,
@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
 
   const int n_last = n - (SPLIT - 1) * L;  // tiles of the last part (<= L)
   // the key tile that holds the ragged end of the sequence, if this workgroup copies one
-  const int t_rag = (S % 32) && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
+  const int t_rag = RAG && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
   // the iteration (in this wave's part) whose tile must be masked: the wave's
   // last tile when it straddles the causal diagonal or the end of the sequence
   // (without the clamp, every tile from the one holding the diagonal on: i >= i_mask)
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       if (p < SPLIT - 1 || x < n_last) {
         const int t = p * L + x;
         char* dst = smem + (p * NB + decltype(slc)::value) * SET;
-        if (t != t_rag) {
+        if (!RAG || t != t_rag) {
           tc.copy_full(Kb, t * 32, dst);
           tc.copy_full(Vb, t * 32, dst + TILE);
         } else {
@@ -234,7 +234,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int key = k0 + acc_row(a, h);
-          if (key >= S || (CAUSAL && key > my_q)) sa_[a] = kMasked;
+          if ((RAG && key >= S) || (CAUSAL && key > my_q)) sa_[a] = kMasked;
         }
       }
       // K of the next tile.  On a wave's last iteration this slot holds another
@@ -359,7 +359,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
 // dS = P (dP - D) takes one multiply per element: the dP contraction starts
 // from an accumulator holding D and multiplies by -dO, so it yields D - dP.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL, int SPLIT, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                                const bf16* __restrict__ V, const bf16* __restrict__ O,
                                                                const bf16* __restrict__ dO,
@@ -398,7 +398,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 
   const int n_last = n - (SPLIT - 1) * L;  // tiles of the last part (<= L)
   // the key tile that holds the ragged end of the sequence, if this workgroup copies one
-  const int t_rag = (S % 32) && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
+  const int t_rag = RAG && (S - 1) / 32 < n ? (S - 1) / 32 : -1;
   // the iteration (in this wave's part) whose tile must be masked: the wave's
   // last tile when it straddles the causal diagonal or the end of the sequence
   // (without the clamp, every tile from the one holding the diagonal on: i >= i_mask)
@@ -413,7 +413,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
       if (p < SPLIT - 1 || x < n_last) {
         const int t = p * L + x;
         char* dst = smem + (p * NB + decltype(slc)::value) * SET;
-        if (t != t_rag) {
+        if (!RAG || t != t_rag) {
           tc.copy_full(Kb, t * 32, dst);
           tc.copy_full(Vb, t * 32, dst + TILE);
         } else {
@@ -485,7 +485,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int key = k0 + acc_row(a, h);
-          if (key >= S || (CAUSAL && key > my_q)) s[a] = kMasked;
+          if ((RAG && key >= S) || (CAUSAL && key > my_q)) s[a] = kMasked;
         }
       }
 #pragma unroll
@@ -562,7 +562,7 @@ template <int D, bool CAUSAL, int SPLIT, int NB>
 constexpr bool dkdv_lean() {
   return CATTN_DKDV_LEAN && D == 64 && SPLIT == 1;
 }
-template <int D, bool CAUSAL, int SPLIT, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(dkdv_lean<D, CAUSAL, SPLIT, NB>() ? 3 : 1, 10)))
 void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
                                                                  const bf16* __restrict__ K,
@@ -622,7 +622,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
   const int i_span = max(0, min(part == SPLIT - 1 ? n_last : L, nt - jb - tb) - i_lo);  // active count
   // causal diagonal (without the clamp, the tiles before it come after it in the walk: i >= i_diag)
   const int i_diag = CAUSAL ? nt - 1 - kw / 32 - tb : -1;
-  const int t_rag = (S % 32) ? 0 : -1;           // walk position of the ragged (last) tile
+  const int t_rag = RAG ? 0 : -1;               // walk position of the ragged (last) tile
   const int i_rag = t_rag - tb;                  // ... in this part
   // copies: iteration x of the ring holds walk position p*L + x of every part p with x < L (x < n_last for the last)
 
@@ -635,7 +635,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
         const int t = p * L + x;
         const int row0 = (nt - 1 - t) * 32;
         char* b = smem + (p * NB + decltype(slc)::value) * BUF;
-        if (t != t_rag) {
+        if (!RAG || t != t_rag) {
           tc.copy_full(Qb, row0, b);
           tc.copy_full(dOb, row0, b + TILE);
         } else {
@@ -711,12 +711,12 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
         dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
       }
       // s[a], dx[a]: S - LSE/scale and D - dP of query 32j + acc_row(a, h), key my_k
-      if ((CAUSAL && kNoClamp ? i >= i_diag : i == i_diag) || i == i_rag) {  // the causal diagonal or the ragged end
+      if ((CAUSAL && kNoClamp ? i >= i_diag : i == i_diag) || (RAG && i == i_rag)) {  // diagonal or ragged end
         const int qs = (nt - 1 - tb - i) * 32;
 #pragma unroll
         for (int a = 0; a < 16; ++a) {
           const int qry = qs + acc_row(a, h);
-          if (qry >= S || (CAUSAL && my_k > qry)) s[a] = kMasked;
+          if ((RAG && qry >= S) || (CAUSAL && my_k > qry)) s[a] = kMasked;
         }
       }
 #pragma unroll
@@ -817,18 +817,18 @@ template <int D> struct BwdCfg {
   static constexpr int NB_DKDV = D == 64 ? CATTN_DKDV_NB64 : CATTN_DKDV_NB128;
 };
 
-template <int D, bool CAUSAL, int SPLIT, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 static hipError_t launch_dq(const BwdArgs& a, float c, hipStream_t st) {
   constexpr int BQ = 128 / SPLIT;
   const int n_qtiles = (a.S + BQ - 1) / BQ;
-  hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
+  hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
                      (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, CATTN_BAND, a.H,
                      (int)a.seq_major);
   return hipGetLastError();
 }
 
-template <int D, bool CAUSAL, int SPLIT, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
   constexpr int BKV = 128 / SPLIT;
   const int n_ktiles = (a.S + BKV - 1) / BKV;
@@ -836,24 +836,24 @@ static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
   // from the start (three per CU)
   const int band = CATTN_DKDV_BAND && dkdv_lean<D, CAUSAL, SPLIT, NB>() &&
                            (int64_t)a.BH * n_ktiles <= 3 * (int64_t)cu_count() ? CATTN_BAND : 0;
-  hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
+  hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
                      (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale,
                      band, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 
-template <int D, bool CAUSAL, int SPLIT, int NB>
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 static hipError_t launch_fwd_split(const FwdArgs& a, hipStream_t st) {
   constexpr int BQ = 128 / SPLIT;
   const int n_qtiles = (a.S + BQ - 1) / BQ;
-  hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
+  hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S,
                      a.BH, n_qtiles, a.scale * kLog2e, CATTN_BAND, a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, bool RAG>
 static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
   if constexpr (D == 64) {
     // Split each query tile's key range over two parts when the unsplit grid
@@ -863,17 +863,25 @@ static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
     // the softmax offset from.)
     const bool split = !kNoClamp && (CATTN_FWD_SPLIT_MODE == 1 ||
                        (CATTN_FWD_SPLIT_MODE == 0 && (int64_t)a.BH * ((a.S + 127) / 128) < 3 * (int64_t)cu_count()));
-    if (split) return launch_fwd_split<D, CAUSAL, 2, FwdCfg<D>::NB_SPLIT>(a, st);
+    if (split) return launch_fwd_split<D, CAUSAL, 2, FwdCfg<D>::NB_SPLIT, RAG>(a, st);
   }
-  return launch_fwd_split<D, CAUSAL, 1, FwdCfg<D>::NB>(a, st);
+  return launch_fwd_split<D, CAUSAL, 1, FwdCfg<D>::NB, RAG>(a, st);
+}
+
+// The kernels come in two builds: with the ragged-end handling (S not a
+// multiple of 32: the last tile's rows past S are masked and copied from row
+// S - 1) and without it, so that whole tiles carry no per-tile test for it.
+template <int D, bool CAUSAL>
+static hipError_t fwd_bf16_r(const FwdArgs& a, hipStream_t st) {
+  return a.S % 32 ? fwd_bf16_t<D, CAUSAL, true>(a, st) : fwd_bf16_t<D, CAUSAL, false>(a, st);
 }
 
 hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t st) {
-  if (a.D == 64) return a.causal ? fwd_bf16_t<64, true>(a, st) : fwd_bf16_t<64, false>(a, st);
-  return a.causal ? fwd_bf16_t<128, true>(a, st) : fwd_bf16_t<128, false>(a, st);
+  if (a.D == 64) return a.causal ? fwd_bf16_r<64, true>(a, st) : fwd_bf16_r<64, false>(a, st);
+  return a.causal ? fwd_bf16_r<128, true>(a, st) : fwd_bf16_r<128, false>(a, st);
 }
 
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, bool RAG>
 static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   constexpr int NB = BwdCfg<D>::NB;
   const float c = a.scale * kLog2e;
@@ -888,21 +896,26 @@ static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   if (phase != 2) {
     hipError_t e;
     if constexpr (D == 64) {
-      e = split ? launch_dq<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st) : launch_dq<D, CAUSAL, 1, NB>(a, c, st);
+      e = split ? launch_dq<D, CAUSAL, 2, CATTN_DKDV_NB64S, RAG>(a, c, st) : launch_dq<D, CAUSAL, 1, NB, RAG>(a, c, st);
     } else {
-      e = launch_dq<D, CAUSAL, 1, NB>(a, c, st);
+      e = launch_dq<D, CAUSAL, 1, NB, RAG>(a, c, st);
     }
     if (e != hipSuccess || phase == 1) return e;
   }
   if constexpr (D == 64) {
-    if (split) return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S>(a, c, st);
+    if (split) return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S, RAG>(a, c, st);
   }
-  return launch_dkdv<D, CAUSAL, 1, BwdCfg<D>::NB_DKDV>(a, c, st);
+  return launch_dkdv<D, CAUSAL, 1, BwdCfg<D>::NB_DKDV, RAG>(a, c, st);
+}
+
+template <int D, bool CAUSAL>
+static hipError_t bwd_bf16_r(const BwdArgs& a, int phase, hipStream_t st) {
+  return a.S % 32 ? bwd_bf16_t<D, CAUSAL, true>(a, phase, st) : bwd_bf16_t<D, CAUSAL, false>(a, phase, st);
 }
 
 hipError_t launch_bwd_bf16(const BwdArgs& a, int phase, hipStream_t st) {
-  if (a.D == 64) return a.causal ? bwd_bf16_t<64, true>(a, phase, st) : bwd_bf16_t<64, false>(a, phase, st);
-  return a.causal ? bwd_bf16_t<128, true>(a, phase, st) : bwd_bf16_t<128, false>(a, phase, st);
+  if (a.D == 64) return a.causal ? bwd_bf16_r<64, true>(a, phase, st) : bwd_bf16_r<64, false>(a, phase, st);
+  return a.causal ? bwd_bf16_r<128, true>(a, phase, st) : bwd_bf16_r<128, false>(a, phase, st);
 }
 
 }  // namespace cattn
