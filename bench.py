@@ -8,9 +8,12 @@ FLOPs of the step (forward 2*B*H*S^2*D, backward 5*B*H*S^2*D) over the wall
 time of exactly --steps steps, bracketed by device synchronisations.
 
 The same timed region also records HIP events around each kernel, on the
-stream the kernels run on, on every 8th step (--event-every); the slowest
-kernel's mean duration over those launches gives the roofline entry.  After
-the timed region every workload (the tiny float32 one, GPT-2 small/medium, XL
+stream the kernels run on, on every 8th step (--event-every; at least 8 steps
+are sampled); the slowest kernel's mean duration over those launches gives the
+roofline entry, beside the same kernel's mean duration in the committed
+rocprofv3 kernel trace.  After the timed region the step is timed again
+--repeats times (median reported) and with the last-level cache evicted before
+each step (--cold), and every workload (the tiny float32 one, GPT-2 small/medium, XL
 width, long context, and GPT-2 small stored [B, S, H, D]) is timed too --
 forward, backward and whole step -- under "configs", and shapes across the
 paper's attention sweep under "sweep", the fused loss head under "lmhead" and
@@ -297,6 +300,70 @@ def time_memops(wl, bd, steps: int, warmup: int):
     return out
 
 
+def measured_trace_us(kernel: str, workload: str):
+    """Mean duration (us) of `kernel` on `workload` in the committed rocprofv3
+    kernel-trace summary, or None when there is none or the kernel sources
+    changed since it was taken."""
+    path = os.path.join(PROFILES, f"kernel_trace_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    digest, us = None, None
+    names = {"attn_fwd": "attn_fwd_bf16_kernel", "attn_bwd_dq": "attn_bwd_dq_bf16_kernel",
+             "attn_bwd_dkdv": "attn_bwd_dkdv_bf16_kernel"}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("# kernel_sources_sha256:"):
+                digest = line.split(":", 1)[1].strip()
+            elif not line.startswith("#") and line.strip().startswith(names.get(kernel, "?")):
+                us = float(line.split()[-4])  # columns after the name: calls, avg_us, min_us, max_us, pct
+    return us if digest == kernel_source_digest() else None
+
+
+def time_repeats(kernels, stream, repeats: int, steps: int, flops: float):
+    """The step timed `repeats` more times, `steps` steps each, between device
+    synchronisations (no events): median and spread of ms per step."""
+    import statistics
+    import torch
+    ms = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            for _, f in kernels:
+                f()
+        torch.cuda.synchronize()
+        ms.append((time.perf_counter() - t0) * 1e3 / steps)
+    med = statistics.median(ms)
+    return {"repeats": repeats, "steps_each": steps, "ms_per_step": [round(x, 5) for x in ms],
+            "median_ms_per_step": round(med, 5), "median_tflops": round(flops / (med * 1e-3) / 1e12, 2)}
+
+
+def time_cold(kernels, stream, steps: int, flops: float, peak: float):
+    """The step with the 256 MB last-level cache (MALL) evicted before every
+    step: 512 MB are written between steps.  Each step is bracketed by HIP
+    events on the kernels' stream, so the eviction writes are not timed."""
+    import torch
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+    times = []
+    for i in range(steps + 1):
+        flush.fill_(i & 0xFF)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _, f in kernels:
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if i > 0:
+            times.append(e0.elapsed_time(e1))
+    times.sort()
+    med = times[len(times) // 2]
+    del flush
+    return {"steps": steps, "evicted_bytes_between_steps": 512 << 20, "median_ms_per_step": round(med, 5),
+            "median_tflops": round(flops / (med * 1e-3) / 1e12, 2),
+            "pct_mfma_peak": round(100.0 * flops / (med * 1e-3) / 1e12 / peak, 2),
+            "note": "each step bracketed by HIP events (dispatch latency of the first kernel included)"}
+
+
 def copy_probe(mib: int) -> int:
     """A plain copy of known size: it reads and writes exactly mib MiB per launch."""
     import torch
@@ -322,6 +389,12 @@ def main() -> int:
                     help="budget of the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--configs", type=int, default=1,
                     help="also time every workload (forward, backward, step) after the timed region (0 disables)")
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="after the timed region, time the step this many more times (median reported; 0 disables)")
+    ap.add_argument("--repeat-steps", type=int, default=100, help="steps per repeat")
+    ap.add_argument("--cold", type=int, default=1,
+                    help="also time the step with the 256 MB MALL evicted (512 MB written) before each step")
+    ap.add_argument("--cold-steps", type=int, default=20, help="steps of the cold variant")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark, run 5 plain device-to-device copies of this many MiB "
                          "(reference kernel for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -392,7 +465,8 @@ def main() -> int:
     # kernels' stream; the other steps run bare.  An event between two kernels
     # costs the GPU a few microseconds, so recording them on every step would
     # inflate the step time the throughput is computed from by about a tenth.
-    every = max(1, args.event_every)
+    # at least 8 sampled steps whenever the run has that many
+    every = max(1, min(args.event_every, args.steps // 8))
     sampled = [i for i in range(args.steps) if i % every == 0]
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)] for _ in sampled]
     torch.cuda.synchronize()
@@ -420,10 +494,15 @@ def main() -> int:
     kf = kernel_flops(w)
     dom = max(per_kernel_ms, key=per_kernel_ms.get)
     achieved = kf[dom] / (per_kernel_ms[dom] * 1e-3) / 1e12
+    trace_us = measured_trace_us(dom, w.name)
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name), "kernel": dom,
                 "flops_per_launch": kf[dom], "mean_launch_us": round(per_kernel_ms[dom] * 1e3, 2),
-                "timed_launches": len(ev)}
+                "timed_launches": len(ev),
+                # the same kernel's mean duration in the committed rocprofv3 kernel trace (no event marker
+                # before the launch, so no dispatch latency in it), while the kernel sources are unchanged
+                "trace_mean_launch_us": trace_us,
+                "frac_from_trace": round(kf[dom] / (trace_us * 1e-6) / 1e12 / peak, 4) if trace_us else None}
 
     line = {
         "metric": METRIC,
@@ -444,6 +523,10 @@ def main() -> int:
         "kernels_us": {n: round(t * 1e3, 2) for n, t in per_kernel_ms.items()},
         "roofline": roofline,
     }
+    if args.repeats > 0:
+        line["repeats"] = time_repeats(kernels, stream, args.repeats, args.repeat_steps, fwd_f + bwd_f)
+    if args.cold:
+        line["cold"] = time_cold(kernels, stream, args.cold_steps, fwd_f + bwd_f, peak)
     if args.configs:
         from paper_2608_00029_amd.workloads import SWEEP, WORKLOADS
         line["configs"] = {c.name: time_workload(c, bd, steps=20, warmup=5) for c in WORKLOADS}

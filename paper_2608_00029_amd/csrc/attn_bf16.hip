@@ -31,47 +31,21 @@
 
 namespace cattn {
 
-// Ring depths (buffers of 32-row tiles).  The forward at D = 64 runs two key
-// parts per workgroup, each with its own ring.
-#ifndef CATTN_FWD_NB64
-#define CATTN_FWD_NB64 3
-#endif
-#ifndef CATTN_FWD_NB128
-#define CATTN_FWD_NB128 4
-#endif
-#ifndef CATTN_BWD_NB64
-#define CATTN_BWD_NB64 6
-#endif
-#ifndef CATTN_BWD_NB128
-#define CATTN_BWD_NB128 4
-#endif
-#ifndef CATTN_FWD_SPLIT_MODE  // forward key split at D = 64: 0 by grid size, 1 always, 2 never
-#define CATTN_FWD_SPLIT_MODE 0
-#endif
-#ifndef CATTN_BWD_SPLIT_WG_PER_CU  // backward at D = 64: split below this many unsplit workgroups per CU
-#define CATTN_BWD_SPLIT_WG_PER_CU 2
-#endif
-#ifndef CATTN_BAND  // rounds of work groups dealt in alternating directions (0: plain heaviest-first)
-#define CATTN_BAND cu_count()
-#endif
-#ifndef CATTN_DKDV_NB64  // dK/dV ring depth at D = 64 (unsplit)
-#define CATTN_DKDV_NB64 CATTN_BWD_NB64
-#endif
-#ifndef CATTN_DKDV_NB128  // dK/dV ring depth at D = 128
-#define CATTN_DKDV_NB128 CATTN_BWD_NB128
-#endif
-#ifndef CATTN_DKDV_GROUP  // iterations per barrier of the unsplit rings (where the ring is deep enough)
-#define CATTN_DKDV_GROUP 3
-#endif
-#ifndef CATTN_DQ_GROUP
-#define CATTN_DQ_GROUP 3
-#endif
-#ifndef CATTN_FWD_GROUP
-#define CATTN_FWD_GROUP 2
-#endif
-#ifndef CATTN_DKDV_NB64S  // dQ and dK/dV at D = 64 with the loop range split in two (two rings)
-#define CATTN_DKDV_NB64S 4
-#endif
+// Ring depths (LDS slots of 32-row tiles) and iterations per ring barrier, as
+// measured best on the MI355X.  Unsplit rings at head dimension 64 (forward, dQ
+// and dK/dV) hold 6 tiles: with three work groups per CU that is 144 of the
+// CU's 160 KB of LDS.
+constexpr int kNb64 = 6;
+constexpr int kFwdNb128 = 4;     // forward at head dimension 128
+constexpr int kBwdNb128 = 4;     // dQ and dK/dV at head dimension 128
+constexpr int kFwdNbSplit = 3;   // forward at D = 64 with the key range in two parts (one ring each)
+constexpr int kBwdNbSplit = 4;   // dQ and dK/dV at D = 64 with the loop range in two parts
+constexpr int kFwdGroup = 2;     // iterations per barrier, where the ring is deep enough (ring_group)
+constexpr int kDqGroup = 3;
+constexpr int kDkdvGroup = 3;
+// The backward at D = 64 splits each tile's loop range in two when the unsplit
+// grid would fill fewer than this many work-group slots per CU.
+constexpr int kBwdSplitWgPerCu = 2;
 
 // Causal loop clamping (section 4.2): the loops visit only the tiles that hold
 // visible (query, key) pairs -- the forward and dQ loops stop at the diagonal,
@@ -174,7 +148,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
     }
   };
   constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
-  constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_FWD_GROUP);  // iterations per barrier
+  constexpr int GROUP = ring_group(SPLIT, NB, NEED, kFwdGroup);  // iterations per barrier
   ring_prologue<NB, GROUP>(L, dma);
   MB::frag qf[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
@@ -424,7 +398,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
     }
   };
   constexpr int NEED = 0;  // iteration i reads the tiles of iterations i .. i+NEED
-  constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_DQ_GROUP);  // iterations per barrier
+  constexpr int GROUP = ring_group(SPLIT, NB, NEED, kDqGroup);  // iterations per barrier
   ring_prologue<NB, GROUP>(L, dma);
   MB::frag qf[KS_D], dof[KS_D], of[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
@@ -552,15 +526,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 // diagonal, the ragged tile), and every wave issues the same copies per tile,
 // so that the common wait at the barrier is a compile-time count.
 // ---------------------------------------------------------------------------
-#ifndef CATTN_DKDV_BAND  // dK/dV work groups dealt in alternating directions per round (as the forward and dQ)
-#define CATTN_DKDV_BAND 1
-#endif
-#ifndef CATTN_DKDV_LEAN  // dK/dV at D = 64, unsplit: operands read where used, three waves per SIMD
-#define CATTN_DKDV_LEAN 1
-#endif
+// dK/dV at D = 64, unsplit: operands read where they are used instead of one
+// tile ahead, which gives three waves per SIMD.
 template <int D, bool CAUSAL, int SPLIT, int NB>
 constexpr bool dkdv_lean() {
-  return CATTN_DKDV_LEAN && D == 64 && SPLIT == 1;
+  return D == 64 && SPLIT == 1;
 }
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(dkdv_lean<D, CAUSAL, SPLIT, NB>() ? 3 : 1, 10)))
@@ -649,7 +619,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
   constexpr int NEED = LEAN ? 0 : 1;  // iteration i reads the tiles of iterations i .. i+NEED
   // With one part, the waves meet at a barrier every GROUP iterations: a wave
   // that runs late on its SIMD then holds the others back less often.
-  constexpr int GROUP = ring_group(SPLIT, NB, NEED, CATTN_DKDV_GROUP);
+  constexpr int GROUP = ring_group(SPLIT, NB, NEED, kDkdvGroup);
   ring_prologue<NB, GROUP>(L, dma);
   MB::frag kf[KS_D], vf[KS_D];
   load_row_frags<bf16, D>(K + base, my_k, S, h, rs, kf);
@@ -809,12 +779,11 @@ static int cu_count() {
 // Forward ring depths: per key part when the key range is split in two (two
 // rings of 3 fit the LDS budget of three workgroups per CU), and unsplit.
 template <int D> struct FwdCfg {
-  static constexpr int NB_SPLIT = CATTN_FWD_NB64;
-  static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_FWD_NB128;
+  static constexpr int NB_SPLIT = kFwdNbSplit;
+  static constexpr int NB = D == 64 ? kNb64 : kFwdNb128;
 };
 template <int D> struct BwdCfg {
-  static constexpr int NB = D == 64 ? CATTN_BWD_NB64 : CATTN_BWD_NB128;
-  static constexpr int NB_DKDV = D == 64 ? CATTN_DKDV_NB64 : CATTN_DKDV_NB128;
+  static constexpr int NB = D == 64 ? kNb64 : kBwdNb128;
 };
 
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
@@ -823,7 +792,7 @@ static hipError_t launch_dq(const BwdArgs& a, float c, hipStream_t st) {
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
-                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, CATTN_BAND, a.H,
+                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, cu_count(), a.H,
                      (int)a.seq_major);
   return hipGetLastError();
 }
@@ -834,8 +803,8 @@ static hipError_t launch_dkdv(const BwdArgs& a, float c, hipStream_t st) {
   const int n_ktiles = (a.S + BKV - 1) / BKV;
   // dealt in alternating directions only when every work group is resident
   // from the start (three per CU)
-  const int band = CATTN_DKDV_BAND && dkdv_lean<D, CAUSAL, SPLIT, NB>() &&
-                           (int64_t)a.BH * n_ktiles <= 3 * (int64_t)cu_count() ? CATTN_BAND : 0;
+  const int band = dkdv_lean<D, CAUSAL, SPLIT, NB>() && (int64_t)a.BH * n_ktiles <= 3 * (int64_t)cu_count()
+                       ? cu_count() : 0;
   hipLaunchKernelGGL((attn_bwd_dkdv_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_ktiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.dout,
                      (const float*)a.ws, (bf16*)a.dk, (bf16*)a.dv, a.S, a.BH, n_ktiles, c, a.scale,
@@ -849,7 +818,7 @@ static hipError_t launch_fwd_split(const FwdArgs& a, hipStream_t st) {
   const int n_qtiles = (a.S + BQ - 1) / BQ;
   hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
                      dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (bf16*)a.o, a.lse, a.S,
-                     a.BH, n_qtiles, a.scale * kLog2e, CATTN_BAND, a.H, (int)a.seq_major);
+                     a.BH, n_qtiles, a.scale * kLog2e, cu_count(), a.H, (int)a.seq_major);
   return hipGetLastError();
 }
 
@@ -861,8 +830,7 @@ static hipError_t fwd_bf16_t(const FwdArgs& a, hipStream_t st) {
     // (The no-clamp test build never splits: a split part would then start on
     // tiles that are fully masked for its queries, with no real score to set
     // the softmax offset from.)
-    const bool split = !kNoClamp && (CATTN_FWD_SPLIT_MODE == 1 ||
-                       (CATTN_FWD_SPLIT_MODE == 0 && (int64_t)a.BH * ((a.S + 127) / 128) < 3 * (int64_t)cu_count()));
+    const bool split = !kNoClamp && (int64_t)a.BH * ((a.S + 127) / 128) < 3 * (int64_t)cu_count();
     if (split) return launch_fwd_split<D, CAUSAL, 2, FwdCfg<D>::NB_SPLIT, RAG>(a, st);
   }
   return launch_fwd_split<D, CAUSAL, 1, FwdCfg<D>::NB, RAG>(a, st);
@@ -892,20 +860,20 @@ static hipError_t bwd_bf16_t(const BwdArgs& a, int phase, hipStream_t st) {
   // overhead per unit of work.
   bool split = false;
   if constexpr (D == 64)
-    split = !kNoClamp && (int64_t)a.BH * ((a.S + 127) / 128) < CATTN_BWD_SPLIT_WG_PER_CU * (int64_t)cu_count();
+    split = !kNoClamp && (int64_t)a.BH * ((a.S + 127) / 128) < kBwdSplitWgPerCu * (int64_t)cu_count();
   if (phase != 2) {
     hipError_t e;
     if constexpr (D == 64) {
-      e = split ? launch_dq<D, CAUSAL, 2, CATTN_DKDV_NB64S, RAG>(a, c, st) : launch_dq<D, CAUSAL, 1, NB, RAG>(a, c, st);
+      e = split ? launch_dq<D, CAUSAL, 2, kBwdNbSplit, RAG>(a, c, st) : launch_dq<D, CAUSAL, 1, NB, RAG>(a, c, st);
     } else {
       e = launch_dq<D, CAUSAL, 1, NB, RAG>(a, c, st);
     }
     if (e != hipSuccess || phase == 1) return e;
   }
   if constexpr (D == 64) {
-    if (split) return launch_dkdv<D, CAUSAL, 2, CATTN_DKDV_NB64S, RAG>(a, c, st);
+    if (split) return launch_dkdv<D, CAUSAL, 2, kBwdNbSplit, RAG>(a, c, st);
   }
-  return launch_dkdv<D, CAUSAL, 1, BwdCfg<D>::NB_DKDV, RAG>(a, c, st);
+  return launch_dkdv<D, CAUSAL, 1, BwdCfg<D>::NB, RAG>(a, c, st);
 }
 
 template <int D, bool CAUSAL>

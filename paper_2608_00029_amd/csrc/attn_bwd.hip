@@ -30,7 +30,7 @@
 namespace cattn {
 
 template <typename T, int D, bool CAUSAL>
-__global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_kernel(const T* __restrict__ Q, const T* __restrict__ K,
+__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                           const T* __restrict__ V, const T* __restrict__ O,
                                                           const T* __restrict__ dO, const float* __restrict__ LSE,
                                                           T* __restrict__ dQ, float* __restrict__ Dvec, int S,
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DQ) void attn_bwd_dq_
 }
 
 template <typename T, int D, bool CAUSAL>
-__global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_DKDV) void attn_bwd_dkdv_kernel(const T* __restrict__ Q, const T* __restrict__ K,
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                             const T* __restrict__ V, const T* __restrict__ dO,
                                                             const float* __restrict__ LSE,
                                                             const float* __restrict__ Dvec, T* __restrict__ dK,

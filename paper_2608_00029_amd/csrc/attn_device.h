@@ -22,18 +22,6 @@
 
 #include "attn_sched.h"
 
-// Occupancy targets (waves per SIMD) handed to the register allocator.
-#ifndef CATTN_WPE_FWD
-#define CATTN_WPE_FWD 0
-#endif
-#ifndef CATTN_WPE_DQ
-#define CATTN_WPE_DQ 0
-#endif
-#ifndef CATTN_WPE_DKDV
-#define CATTN_WPE_DKDV 0
-#endif
-#define CATTN_WPE_ATTR(n) __attribute__((amdgpu_waves_per_eu((n) > 0 ? (n) : 1, (n) > 0 ? (n) : 10)))
-
 namespace cattn {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));

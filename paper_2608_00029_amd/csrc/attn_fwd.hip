@@ -19,7 +19,7 @@
 namespace cattn {
 
 template <typename T, int D, bool CAUSAL>
-__global__ __launch_bounds__(256) CATTN_WPE_ATTR(CATTN_WPE_FWD) void attn_fwd_kernel(const T* __restrict__ Q, const T* __restrict__ K,
+__global__ __launch_bounds__(256) void attn_fwd_kernel(const T* __restrict__ Q, const T* __restrict__ K,
                                                        const T* __restrict__ V, T* __restrict__ O,
                                                        float* __restrict__ LSE, int S, int BH, int n_qtiles,
                                                        float c, int H, int seq_major) {
