@@ -106,19 +106,36 @@ __global__ __launch_bounds__(512) void lmhead_logits_stats_kernel(const bf16* __
         dma(tile_next, 0, slot ^ 1);
       }
       if (active) {
+        // Operand fragments are double-buffered across k-steps: the reads of
+        // step ks + 1 are issued before the contractions of step ks, so each
+        // group of eight contractions runs while the next group's operands
+        // arrive instead of waiting on LDS every two contractions.
         const char* b = smem + slot * SLOT;
+        MB::frag wf[2][4], xf[2][2];
+        auto read_step = [&](int ks, int buf) {
+#pragma unroll
+          for (int a = 0; a < 4; ++a) wf[buf][a] = read_row_frag<bf16, kLmhKC>(b + (4 * vw + a) * TILE, r, ks, h);
+#pragma unroll
+          for (int t = 0; t < 2; ++t) xf[buf][t] = read_row_frag<bf16, kLmhKC>(b + (8 + 2 * tw + t) * TILE, r, ks, h);
+        };
+        read_step(0, 0);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          MB::frag wf[4], xf[2];
-#pragma unroll
-          for (int a = 0; a < 4; ++a) wf[a] = read_row_frag<bf16, kLmhKC>(b + (4 * vw + a) * TILE, r, ks, h);
-#pragma unroll
-          for (int t = 0; t < 2; ++t) xf[t] = read_row_frag<bf16, kLmhKC>(b + (8 + 2 * tw + t) * TILE, r, ks, h);
+          if (ks + 1 < KS) read_step(ks + 1, (ks + 1) & 1);
 #pragma unroll
           for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int t = 0; t < 2; ++t) acc[a][t] = MB::run(wf[a], xf[t], acc[a][t]);
+            for (int t = 0; t < 2; ++t) acc[a][t] = MB::run(wf[ks & 1][a], xf[ks & 1][t], acc[a][t]);
         }
+        // issue order: steps 0 and 1's reads, then per step its eight
+        // contractions followed by the reads two steps ahead
+        static_assert(KS == 4, "the issue order below is written for four k-steps");
+        __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
       }
       slot ^= 1;
     }
