@@ -295,9 +295,34 @@ def time_memops(wl, bd, steps: int, warmup: int):
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps
         gbs = ab / (ms * 1e-3) / 1e9
+        cgbs = copy_gbs(ab)
         out[name] = {"ms": round(ms, 5), "gbs_algorithmic": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 3),
-                     "gbs_paper_bytes": round(nb / (ms * 1e-3) / 1e9, 1), "bytes_algorithmic": ab}
+                     "gbs_paper_bytes": round(nb / (ms * 1e-3) / 1e9, 1), "bytes_algorithmic": ab,
+                     "copy_gbs_same_bytes": round(cgbs, 1), "frac_of_copy": round(gbs / cgbs, 3)}
     return out
+
+
+def copy_gbs(nbytes: int, reps: int = 10) -> float:
+    """Read + write bandwidth of torch's device-to-device copy moving the same
+    number of bytes (nbytes / 2 read, nbytes / 2 written).  A reference point
+    for a kernel that streams its bytes once, not a roof: kernels whose
+    streams are read-only, or written with non-temporal stores, exceed it."""
+    import torch
+    n = max(1, nbytes // 8)
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 8 * n / (ms * 1e-3) / 1e9
 
 
 def measured_trace_us(kernel: str, workload: str):
