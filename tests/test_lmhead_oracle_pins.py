@@ -79,6 +79,39 @@ def test_error_bound_holds_for_float32_accumulation():
     assert np.all(err <= lm.dot_error_bound(x, w))
 
 
+def test_error_bound_is_reached_by_a_worst_case_sum():
+    """The bound is not loose in the worst case: with products 1, t, t, ... and
+    t = 2^-24 (1 + 2^-7) (a bf16 value just above half an ulp of the running
+    sum), every float32 addition of a left-to-right sum rounds up by almost
+    u = 2^-24 of the sum, so the error reaches 99% of gamma_K sum|p|."""
+    K = 768
+    t = 2.0 ** -24 * (1 + 2.0 ** -7)
+    x = np.ones((1, K))
+    w = np.full((1, K), t)
+    w[0, 0] = 1.0
+    assert np.array_equal(torch.tensor(w).to(torch.bfloat16).double().numpy(), w)  # bf16 values
+    z32 = np.cumsum((x[0] * w[0]).astype(np.float32), dtype=np.float32)[-1]
+    assert z32 == np.float32(1 + (K - 1) * 2.0 ** -23)  # every addition rounded up
+    err = abs(float(z32) - float(lm.logits(x, w)[0, 0]))
+    bound = float(lm.dot_error_bound(x, w)[0, 0])
+    assert 0.98 * bound < err <= bound
+
+
+def test_logit_tolerance_catches_plausible_mistakes():
+    """The GPU test holds logits to twice the bound.  On inputs shaped like the
+    loss head's (hidden states N(0, 1), weights N(0, 0.02^2), K = 768), that
+    tolerance still fails logits rounded to bf16 and logits missing one
+    16-wide contraction step, the kind of mistake a kernel could make."""
+    x = torch.tensor(_rand((16, 768), 21)).to(torch.bfloat16).double().numpy()
+    w = torch.tensor(_rand((256, 768), 22, 0.02)).to(torch.bfloat16).double().numpy()
+    z = lm.logits(x, w)
+    tol = 2 * lm.dot_error_bound(x, w)
+    z_bf16 = torch.tensor(z).to(torch.bfloat16).double().numpy()
+    assert np.mean(np.abs(z_bf16 - z) > tol) > 0.05
+    z_short = lm.logits(x[:, 16:], w[:, 16:])
+    assert np.mean(np.abs(z_short - z) > tol) > 0.9
+
+
 def _planted(kind):
     """Copies of oracle steps with one plausible mistake each."""
     def merge_no_rescale(pm, ps):
