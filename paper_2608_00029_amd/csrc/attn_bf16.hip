@@ -533,7 +533,7 @@ constexpr bool dkdv_lean() {
   return D == 64 && SPLIT == 1;
 }
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(dkdv_lean<D, CAUSAL, SPLIT, NB>() ? 3 : 1, 10)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(dkdv_lean<D, CAUSAL, SPLIT, NB>() ? 3 : (D == 128 ? 2 : 1), 10)))
 void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
                                                                  const bf16* __restrict__ K,
                                                                  const bf16* __restrict__ V,
@@ -544,10 +544,20 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
                                                                  int H, int seq_major) {
   typedef TileGeom<D> G;
   constexpr bool LEAN = dkdv_lean<D, CAUSAL, SPLIT, NB>();
+  // D = 128: every operand fragment read from LDS one contraction step before
+  // its use, so that the K, V, dK and dV fragments (192 registers) and the two
+  // score blocks leave room for two waves per SIMD
+  constexpr bool STREAM = D == 128 && SPLIT == 1;
   constexpr int KG = 4 / SPLIT, BKV = 32 * KG;
   constexpr int TILE = G::TILE;
   constexpr int KS_D = D / 16, DT = D / 32;
-  constexpr int BUF = 2 * TILE + 2 * 32 * 4;  // Q, dO, then 32 floats -LSE/scale, 32 floats D
+  // LDS: the Q and dO tiles of every slot first, then the 32 floats of
+  // -LSE/scale and the 32 of D of every slot, so that every tile read of the
+  // ring lies within the 64 KB an LDS instruction's immediate offset reaches
+  // from one per-lane base address (one address register per fragment for
+  // all slots: at D = 128 this keeps the kernel at two waves per SIMD).
+  constexpr int SETB = 2 * TILE, AUX = 2 * 32 * 4, AUX0 = SPLIT * NB * SETB;
+  constexpr int BUF = SETB + AUX;
   // copies per part tile issued by every wave: its share of Q and dO, and 4 of the 16 LSE/D chunks
   constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR + 1;
   __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * BUF];  // [part][slot]
@@ -604,7 +614,7 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
       if (p < SPLIT - 1 || x < n_last) {
         const int t = p * L + x;
         const int row0 = (nt - 1 - t) * 32;
-        char* b = smem + (p * NB + decltype(slc)::value) * BUF;
+        char* b = smem + (p * NB + decltype(slc)::value) * SETB;
         if (!RAG || t != t_rag) {
           tc.copy_full(Qb, row0, b);
           tc.copy_full(dOb, row0, b + TILE);
@@ -612,11 +622,11 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
           tc.copy(Qb, row0, S, b);
           tc.copy(dOb, row0, S, b + TILE);
         }
-        if (lane < 4) dma16(wsh + row0, ld_voff, lds_addr(b + 2 * TILE) + 64 * w);
+        if (lane < 4) dma16(wsh + row0, ld_voff, lds_addr(smem + AUX0 + (p * NB + decltype(slc)::value) * AUX) + 64 * w);
       }
     }
   };
-  constexpr int NEED = LEAN ? 0 : 1;  // iteration i reads the tiles of iterations i .. i+NEED
+  constexpr int NEED = LEAN || STREAM ? 0 : 1;  // iteration i reads the tiles of iterations i .. i+NEED
   // With one part, the waves meet at a barrier every GROUP iterations: a wave
   // that runs late on its SIMD then holds the others back less often.
   constexpr int GROUP = ring_group(SPLIT, NB, NEED, kDkdvGroup);
@@ -636,7 +646,10 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
     dvacc[dt] = f32x16{};
   }
   MB::frag qf[KS_D], dof[KS_D];  // row fragments of the current sub-block
-  const char* ring = smem + part * NB * BUF;
+  Frag128 fo;
+  if constexpr (STREAM) fo.init(r, h, lane);
+  const char* ring = smem + part * NB * SETB;
+  const char* aux = smem + AUX0 + part * NB * AUX;
 
   for (int i0 = 0; i0 < L; i0 += NB) {
     unroll<NB>([&](auto slc) {
@@ -645,24 +658,24 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
       if (i >= L) return;
       ring_step<NB, GROUP, NEED, SPLIT, PER_TILE, sl>(i, L, n_last, dma);
       if ((unsigned)(i - i_lo) >= (unsigned)i_span) return;  // wave-uniform: not an active sub-block
-      const char* lq = ring + sl * BUF;
+      const char* lq = ring + sl * SETB;
       const char* ldo = lq + TILE;
-      const float* llse = (const float*)(lq + 2 * TILE);
+      const float* llse = (const float*)(aux + sl * AUX);
       const float* ld = llse + 32;
       MB::frag dotr[2][DT], qtr[2][DT];
       MB::frag qn[KS_D], don[KS_D];  // next tile of the part (on a wave's last tile: discarded)
       if constexpr (LEAN) {
         read_rows<D>(lq, r, h, qf);
         read_rows<D>(ldo, r, h, dof);
-      } else {
+      } else if constexpr (!STREAM) {
         if (i == i_lo) {  // a wave's first sub-block: read it here
           read_rows<D>(lq, r, h, qf);
           read_rows<D>(ldo, r, h, dof);
         }
         read_trans<D>(ldo, lane, dotr);
         read_trans<D>(lq, lane, qtr);
-        read_rows<D>(ring + sn * BUF, r, h, qn);
-        read_rows<D>(ring + sn * BUF + TILE, r, h, don);
+        read_rows<D>(ring + sn * SETB, r, h, qn);
+        read_rows<D>(ring + sn * SETB + TILE, r, h, don);
       }
       f32x16 s, dx;
 #pragma unroll
@@ -675,10 +688,25 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
           dx[4 * g + e] = d4[e];
         }
       }
+      if constexpr (STREAM) {
+        MB::frag qa[2], da[2];
+        qa[0] = fo.row_frag(lq, 0);
+        da[0] = fo.row_frag(ldo, 0);
 #pragma unroll
-      for (int ks = 0; ks < KS_D; ++ks) {
-        s = MB::run(qf[ks], kf[ks], s);
-        dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
+        for (int ks = 0; ks < KS_D; ++ks) {
+          if (ks + 1 < KS_D) {
+            qa[(ks + 1) & 1] = fo.row_frag(lq, ks + 1);
+            da[(ks + 1) & 1] = fo.row_frag(ldo, ks + 1);
+          }
+          s = MB::run(qa[ks & 1], kf[ks], s);
+          dx = MB::run(da[ks & 1], vf[ks], dx);  // D - dP
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < KS_D; ++ks) {
+          s = MB::run(qf[ks], kf[ks], s);
+          dx = MB::run(dof[ks], vf[ks], dx);  // D - dP
+        }
       }
       // s[a], dx[a]: S - LSE/scale and D - dP of query 32j + acc_row(a, h), key my_k
       if ((CAUSAL && kNoClamp ? i >= i_diag : i == i_diag) || (RAG && i == i_rag)) {  // diagonal or ragged end
@@ -699,17 +727,41 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
         read_trans<D>(ldo, lane, dotr);
         read_trans<D>(lq, lane, qtr);
       }
+      if constexpr (STREAM) {
+        // P and dS packed first, so that their float forms are dead before the
+        // transposed fragments are read
+        const MB::frag pb[2] = {MB::pack(s, 0), MB::pack(s, 1)};
+        const MB::frag db[2] = {MB::pack(dx, 0), MB::pack(dx, 1)};
+        MB::frag ta[2], tq[2];
+        ta[0] = fo.trans(ldo, 0, 0);
+        tq[0] = fo.trans(lq, 0, 0);
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const MB::frag pb = MB::pack(s, ks);
-        const MB::frag db = MB::pack(dx, ks);
+        for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          dvacc[dt] = MB::run(dotr[ks][dt], pb, dvacc[dt]);
-          dkacc[dt] = MB::run(qtr[ks][dt], db, dkacc[dt]);
+          for (int dt = 0; dt < DT; ++dt) {
+            const int x = ks * DT + dt;
+            if (x + 1 < 2 * DT) {
+              const int ks1 = (x + 1) / DT, dt1 = (x + 1) % DT;
+              ta[(x + 1) & 1] = fo.trans(ldo, ks1, dt1);
+              tq[(x + 1) & 1] = fo.trans(lq, ks1, dt1);
+            }
+            dvacc[dt] = MB::run(ta[x & 1], pb[ks], dvacc[dt]);
+            dkacc[dt] = MB::run(tq[x & 1], db[ks], dkacc[dt]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const MB::frag pb = MB::pack(s, ks);
+          const MB::frag db = MB::pack(dx, ks);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            dvacc[dt] = MB::run(dotr[ks][dt], pb, dvacc[dt]);
+            dkacc[dt] = MB::run(qtr[ks][dt], db, dkacc[dt]);
+          }
         }
       }
-      if constexpr (!LEAN) {
+      if constexpr (!LEAN && !STREAM) {
 #pragma unroll
         for (int ks = 0; ks < KS_D; ++ks) {
           qf[ks] = qn[ks];

@@ -207,6 +207,47 @@ __device__ __forceinline__ void read_trans(const char* lds, int lane, MB::frag (
     for (int dt = 0; dt < D / 32; ++dt) f[s][dt] = TransRead<bf16, D>::read(lds, 0, s, dt * 32, lane);
 }
 
+// Fragment reads of a D = 128 tile from per-lane offsets computed once.  The
+// swizzle permutes only bits 0-2 of a row's 16-byte chunk index, so chunk bit 3
+// -- row fragments ks >= 4, transposed fragments of columns 64.. -- is a fixed
+// 128-byte step: 4 offsets serve the 8 row fragments and 8 the 16 transposed
+// halves, each read an offset register plus an immediate (the compiler would
+// otherwise keep one address register per fragment and per ring slot).
+struct Frag128 {
+  typedef Tile<__bf16, 128> T;
+  static_assert(T::kChunks == 16, "row of 16 chunks");
+  unsigned row[4];       // row fragment ks & 3 of row r
+  unsigned tr[2][2][2];  // transposed: [k-step s][rows +8][column block dt & 1]
+  __device__ __forceinline__ void init(int r, int h, int lane) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) row[k] = (unsigned)T::off(r, k * 16 + h * 8);
+    const int g = lane >> 4, hh = g >> 1, m = lane & 15;
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int d = 0; d < 2; ++d)
+          tr[s][e][d] = (unsigned)T::off(16 * s + 4 * hh + (m >> 2) + 8 * e, 32 * d + 16 * (g & 1) + 4 * (m & 3));
+  }
+  __device__ __forceinline__ MB::frag row_frag(const char* tile, int ks) const {
+    return *(const MB::frag*)(tile + row[ks & 3] + (ks >> 2) * 128);
+  }
+  __device__ __forceinline__ MB::frag trans(const char* tile, int s, int dt) const {
+    const int step = (dt >> 1) * 128;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tr[s][0][dt & 1] + step));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tr[s][1][dt & 1] + step));
+    const bf16x4 l4 = __builtin_bit_cast(bf16x4, lo), h4 = __builtin_bit_cast(bf16x4, hi);
+    MB::frag f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[i] = l4[i];
+      f[4 + i] = h4[i];
+    }
+    return f;
+  }
+};
+
 // Flip the sign of every element of a bf16 fragment.
 __device__ __forceinline__ MB::frag negated(MB::frag f) {
   u32x4 u = __builtin_bit_cast(u32x4, f);
