@@ -527,7 +527,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 // so that the common wait at the barrier is a compile-time count.
 // ---------------------------------------------------------------------------
 // dK/dV at D = 64, unsplit: operands read where they are used instead of one
-// tile ahead, which gives three waves per SIMD.
+// tile ahead, which gives three waves per SIMD.  At D = 128 (STREAM below) each
+// operand fragment is read one contraction step before its use, which gives
+// two; split grids at D = 64 read the next tile's rows one tile ahead.
 template <int D, bool CAUSAL, int SPLIT, int NB>
 constexpr bool dkdv_lean() {
   return D == 64 && SPLIT == 1;
@@ -560,8 +562,10 @@ void attn_bwd_dkdv_bf16_kernel(const bf16* __restrict__ Q,
   constexpr int BUF = SETB + AUX;
   // copies per part tile issued by every wave: its share of Q and dO, and 4 of the 16 LSE/D chunks
   constexpr int PER_TILE = 2 * G::DMA_PER_TENSOR + 1;
-  __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * BUF];  // [part][slot]
+  // [part][slot] Q, dO tiles, then [part][slot] -LSE/scale and D rows
+  __shared__ __attribute__((aligned(16))) char smem[SPLIT * NB * BUF];
   static_assert(SPLIT == 1 || KG * 64 * (4 * DT * 16) * 4 <= SPLIT * NB * BUF, "merge area");
+  static_assert(!STREAM || AUX0 <= 65536, "tile reads reach every slot by immediate offset");
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in an SGPR
