@@ -28,9 +28,14 @@ DEV = "cuda:0"
 
 
 def gpu_fwd_bwd(q, k, v, do, scale, causal):
+    """Forward and backward on the GPU into output buffers filled with NaN
+    beforehand, so that a finite output proves every element was written."""
     qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
-    o, lse = attn_fwd(qd, kd, vd, scale, causal)
-    dq, dk, dv = attn_bwd(qd, kd, vd, o, dod, lse, scale, causal)
+    B, H, S, _ = q.shape
+    o, dq, dk, dv = (torch.full_like(qd, float("nan")) for _ in range(4))
+    lse = torch.full((B, H, S), float("nan"), dtype=torch.float32, device=DEV)
+    attn_fwd(qd, kd, vd, scale, causal, o=o, lse=lse)
+    attn_bwd(qd, kd, vd, o, dod, lse, scale, causal, dq=dq, dk=dk, dv=dv)
     torch.cuda.synchronize()
     return tuple(t.cpu() for t in (o, lse, dq, dk, dv))
 
@@ -122,7 +127,7 @@ def test_workload_parity(cuda, w):
     sel = lambda t: torch.stack([t[b, h] for b, h in heads])[None]  # noqa: E731
     qs, ks, vs, dos = (sel(t) for t in (q, k, v, do))
     compare_all(w.dtype, tuple(sel(t) for t in got), qs, ks, vs, dos, w.scale, w.causal)
-    for t in got:
+    for t in got:  # every element of every head written (the buffers started as NaN)
         assert torch.isfinite(t.float()).all()
 
 
