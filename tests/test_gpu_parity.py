@@ -47,7 +47,8 @@ def compare_all(dtype, got, q, k, v, do, scale, causal):
     pairs = (("o", o, ro), ("lse", lse, rlse), ("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv))
     rep = [check_tensor(n, dtype, g, r) for n, g, r in pairs]
     if dtype == "bf16":
-        bounds = bf16_bounds(q, k, orc.attn_term_magnitudes(q, k, v, do, scale, causal), scale, max_abs(lse, rlse))
+        mags = orc.attn_term_magnitudes(q, k, v, do, scale, causal)
+        bounds = bf16_bounds(q, k, v, do, mags, scale, max_abs(lse, rlse))
         rep += [check_bounded(n, g, r, bounds[n]) for n, g, r in pairs if n != "lse"]
     print("  " + "  ".join(rep), flush=True)
 
@@ -173,7 +174,7 @@ def test_bwd_isolated_from_fwd(cuda):
         for n, g, r in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
             check_tensor(n, dtype, g.cpu(), r)
         if dtype == "bf16":
-            bounds = bf16_bounds(q, k, orc.attn_term_magnitudes(q, k, v, do, scale, True), scale,
+            bounds = bf16_bounds(q, k, v, do, orc.attn_term_magnitudes(q, k, v, do, scale, True), scale,
                                  max_abs(lse.cpu(), rlse))
             for n, g, r in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
                 check_bounded(n, g.cpu(), r, bounds[n])
@@ -200,6 +201,39 @@ def test_gpu_invariants(cuda):
     prefix = np.cumsum(to64(v), axis=2) / np.arange(1, 1025)[None, None, :, None]
     assert np.linalg.norm(to64(o0) - prefix) <= 1e-2 * np.linalg.norm(prefix)
     assert np.max(np.abs(to64(lse0) - np.log(np.arange(1, 1025)))) <= 1e-3
+
+
+EXTREME_SCALES = [
+    # D, S, scale: near-uniform attention (scores ~1e-18) and near one-hot attention (score spread
+    # ~30 on the base-2 scale per row, so the lazy offset is moved many times per row)
+    (64, 300, 1e-20),
+    (128, 300, 1e-20),
+    (64, 640, 4.0),
+    (128, 384, 4.0),
+]
+
+
+@pytest.mark.parametrize("case", EXTREME_SCALES, ids=lambda c: "-".join(map(str, c)))
+def test_extreme_scales(cuda, case):
+    """The degenerate ends of the softmax, bf16, causal: element and row bounds
+    (which grow with the score error at large scale) on every output."""
+    D, S, scale = case
+    q, k, v, do = make_inputs(1, 2, S, D, "bf16", seed=5150 + S + D)
+    say(f"extreme scale D={D} S={S} scale={scale}")
+    o, lse, dq, dk, dv = gpu_fwd_bwd(q, k, v, do, scale, True)
+    ro, rlse = orc.attn_fwd(q, k, v, scale, True)
+    rdq, rdk, rdv = orc.attn_bwd(q, k, v, do, scale, True)
+    lse_err = max_abs(lse, rlse)
+    # LSE bound: every score is off by at most scale |q||k| (D + 4) 2^-24 (float32 dot product
+    # and the scaling), the float32 sum of at most S probabilities adds (S + 4) 2^-24, and the
+    # result is rounded (|LSE| 2^-22 covers the base changes)
+    qn, kn = np.linalg.norm(to64(q), axis=-1).max(), np.linalg.norm(to64(k), axis=-1).max()
+    lse_tol = scale * qn * kn * (D + 4) * 2.0 ** -24 + (S + 4) * 2.0 ** -24 + np.abs(rlse).max() * 2.0 ** -22
+    assert lse_err <= lse_tol, (lse_err, lse_tol)
+    bounds = bf16_bounds(q, k, v, do, orc.attn_term_magnitudes(q, k, v, do, scale, True), scale, lse_err)
+    rep = [check_bounded(n, g, r, bounds[n]) for n, g, r in (("o", o, ro), ("dq", dq, rdq), ("dk", dk, rdk),
+                                                              ("dv", dv, rdv))]
+    print("  " + "  ".join(rep + [f"lse maxabs={lse_err:.2e} (bound {lse_tol:.2e})"]), flush=True)
 
 
 def test_deterministic(cuda):
