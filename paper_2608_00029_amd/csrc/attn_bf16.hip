@@ -32,17 +32,19 @@
 namespace cattn {
 
 // Ring depths (LDS slots of 32-row tiles) and iterations per ring barrier, as
-// measured best on the MI355X.  Unsplit rings at head dimension 64 (forward, dQ
-// and dK/dV) hold 6 tiles: with three work groups per CU that is 144 of the
-// CU's 160 KB of LDS.
-constexpr int kNb64 = 6;
+// measured best on the MI355X.  The unsplit forward ring at head dimension 64
+// holds 6 tiles (with three work groups per CU, 144 of the CU's 160 KB of LDS);
+// the backward rings hold 4, copies 3 tiles ahead (6-tile rings measured 2-5%
+// slower in both backward kernels).
+constexpr int kFwdNb64 = 6;      // forward at head dimension 64
+constexpr int kBwdNb64 = 4;      // dQ and dK/dV at head dimension 64
 constexpr int kFwdNb128 = 4;     // forward at head dimension 128
 constexpr int kBwdNb128 = 4;     // dQ and dK/dV at head dimension 128
 constexpr int kFwdNbSplit = 3;   // forward at D = 64 with the key range in two parts (one ring each)
 constexpr int kBwdNbSplit = 4;   // dQ and dK/dV at D = 64 with the loop range in two parts
 constexpr int kFwdGroup = 2;     // iterations per barrier, where the ring is deep enough (ring_group)
-constexpr int kDqGroup = 3;
-constexpr int kDkdvGroup = 3;
+constexpr int kDqGroup = 2;
+constexpr int kDkdvGroup = 2;
 // The backward at D = 64 splits each tile's loop range in two when the unsplit
 // grid would fill fewer than this many work-group slots per CU.
 constexpr int kBwdSplitWgPerCu = 2;
@@ -836,10 +838,10 @@ static int cu_count() {
 // rings of 3 fit the LDS budget of three workgroups per CU), and unsplit.
 template <int D> struct FwdCfg {
   static constexpr int NB_SPLIT = kFwdNbSplit;
-  static constexpr int NB = D == 64 ? kNb64 : kFwdNb128;
+  static constexpr int NB = D == 64 ? kFwdNb64 : kFwdNb128;
 };
 template <int D> struct BwdCfg {
-  static constexpr int NB = D == 64 ? kNb64 : kBwdNb128;
+  static constexpr int NB = D == 64 ? kBwdNb64 : kBwdNb128;
 };
 
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
