@@ -38,7 +38,7 @@ namespace cattn {
 // slower in both backward kernels).
 constexpr int kFwdNb64 = 6;      // forward at head dimension 64
 constexpr int kBwdNb64 = 4;      // dQ and dK/dV at head dimension 64
-constexpr int kFwdNb128 = 4;     // forward at head dimension 128
+constexpr int kFwdNb128 = 3;     // forward at head dimension 128 (three work groups per CU)
 constexpr int kBwdNb128 = 4;     // dQ and dK/dV at head dimension 128
 constexpr int kFwdNbSplit = 3;   // forward at D = 64 with the key range in two parts (one ring each)
 constexpr int kBwdNbSplit = 4;   // dQ and dK/dV at D = 64 with the loop range in two parts
@@ -88,7 +88,8 @@ constexpr float kSumMax = 4294967296.0f;
 // the block.  No per-block max is computed on the common path.
 // ---------------------------------------------------------------------------
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
-__global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 && SPLIT == 1 ? 3 : 1, 10)))
+void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                             const bf16* __restrict__ V, bf16* __restrict__ O,
                                                             float* __restrict__ LSE, int S, int BH, int n_qtiles,
                                                             float c, int band, int H, int seq_major) {
@@ -149,9 +150,17 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       }
     }
   };
-  constexpr int NEED = 1;  // iteration i reads the tiles of iterations i .. i+NEED
+  // D = 128: each block runs start to end in its iteration (no score block
+  // computed ahead) with every K and V fragment read from LDS one contraction
+  // step before its use, so that Q and O (96 registers) leave room for three
+  // waves per SIMD; D = 64 computes S(j+1) while the softmax of S(j) runs.
+  constexpr bool LEANF = D == 128 && SPLIT == 1;
+  constexpr int NEED = LEANF ? 0 : 1;  // iteration i reads the tiles of iterations i .. i+NEED
   constexpr int GROUP = ring_group(SPLIT, NB, NEED, kFwdGroup);  // iterations per barrier
+  static_assert(!LEANF || SPLIT * NB * SET <= 65536, "tile reads reach every slot by immediate offset");
   ring_prologue<NB, GROUP>(L, dma);
+  Frag128 fo;
+  if constexpr (LEANF) fo.init(r, h, lane);
   MB::frag qf[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
   wait_vm(0);
@@ -177,7 +186,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) vf[ks][dt] = MB::frag{};
-  {
+  if constexpr (!LEANF) {
     MB::frag k0f[KS_D];
     read_rows<D>(ring, r, h, k0f);
 #pragma unroll
@@ -203,6 +212,53 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
       if (i >= L) return;
       ring_step<NB, GROUP, NEED, SPLIT, PER_TILE, sl>(i, L, n_last, dma);
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
+      if constexpr (LEANF) {
+        const char* kt = ring + sl * SET;
+        f32x16 s = f32x16{};
+        MB::frag ka[2];
+        ka[0] = fo.row_frag(kt, 0);
+#pragma unroll
+        for (int ks = 0; ks < KS_D; ++ks) {
+          if (ks + 1 < KS_D) ka[(ks + 1) & 1] = fo.row_frag(kt, ks + 1);
+          s = MB::run(ka[ks & 1], qf[ks], s);
+        }
+        if (CAUSAL && kNoClamp ? i >= i_mask : i == i_mask) {
+          const int k0 = (tb + i) * 32;
+#pragma unroll
+          for (int a = 0; a < 16; ++a) {
+            const int key = k0 + acc_row(a, h);
+            if ((RAG && key >= S) || (CAUSAL && key > my_q)) s[a] = kMasked;
+          }
+        }
+        f32x16 pv;
+        float psum = softmax(s, m * c, pv);
+        if (__builtin_amdgcn_ballot_w64(!(psum <= kSumMax))) {  // rare: move the offset
+          asm volatile("" ::: "memory");
+          float mx = s[0];
+#pragma unroll
+          for (int a = 1; a < 16; ++a) mx = fmaxf(mx, s[a]);
+          const float mnew = fmaxf(m, halves_max(mx));
+          const float alpha = exp2_hw((m - mnew) * c);  // 0 on the first block
+          m = mnew;
+          psum = softmax(s, m * c, pv);
+          lsum *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+        }
+        lsum += psum;
+        const MB::frag pb[2] = {MB::pack(pv, 0), MB::pack(pv, 1)};
+        MB::frag va[2];
+        va[0] = fo.trans(kt + TILE, 0, 0);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const int x = ks * DT + dt;
+            if (x + 1 < 2 * DT) va[(x + 1) & 1] = fo.trans(kt + TILE, (x + 1) / DT, (x + 1) % DT);
+            oacc[dt] = MB::run(va[x & 1], pb[ks], oacc[dt]);
+          }
+        return;
+      }
       f32x16& sa_ = sa[pc];
       // causal diagonal / ragged end: only the last tile of the wave's queries
       if (CAUSAL && kNoClamp ? i >= i_mask : i == i_mask) {
@@ -273,7 +329,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const bf16* __restri
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] = MB::run(vf[ks][dt], pl[ks], oacc[dt]);
   };
-  if (cnt > 0) {
+  if (!LEANF && cnt > 0) {
     if (PAR && (cnt & 1)) {
       drain(pp[1]);
     } else {
