@@ -32,11 +32,10 @@
 namespace cattn {
 
 // Ring depths (LDS slots of 32-row tiles) and iterations per ring barrier, as
-// measured best on the MI355X.  The unsplit forward ring at head dimension 64
-// holds 6 tiles (with three work groups per CU, 144 of the CU's 160 KB of LDS);
-// the backward rings hold 4, copies 3 tiles ahead (6-tile rings measured 2-5%
-// slower in both backward kernels).
-constexpr int kFwdNb64 = 6;      // forward at head dimension 64
+// measured best on the MI355X.  The unsplit rings at head dimension 64 hold 4
+// tiles, copies 3 tiles ahead (the forward, at four work groups per CU, uses
+// 128 of the CU's 160 KB of LDS; 6-tile backward rings measured 2-5% slower).
+constexpr int kFwdNb64 = 4;      // forward at head dimension 64
 constexpr int kBwdNb64 = 4;      // dQ and dK/dV at head dimension 64
 constexpr int kFwdNb128 = 3;     // forward at head dimension 128 (three work groups per CU)
 constexpr int kBwdNb128 = 4;     // dQ and dK/dV at head dimension 128
@@ -88,7 +87,7 @@ constexpr float kSumMax = 4294967296.0f;
 // the block.  No per-block max is computed on the common path.
 // ---------------------------------------------------------------------------
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 && SPLIT == 1 ? 3 : 1, 10)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPLIT == 1 ? (D == 128 ? 3 : 4) : 1, 10)))
 void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                             const bf16* __restrict__ V, bf16* __restrict__ O,
                                                             float* __restrict__ LSE, int S, int BH, int n_qtiles,
@@ -150,17 +149,26 @@ void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K
       }
     }
   };
-  // D = 128: each block runs start to end in its iteration (no score block
-  // computed ahead) with every K and V fragment read from LDS one contraction
-  // step before its use, so that Q and O (96 registers) leave room for three
-  // waves per SIMD; D = 64 computes S(j+1) while the softmax of S(j) runs.
-  constexpr bool LEANF = D == 128 && SPLIT == 1;
+  // Unsplit grids: each block runs start to end in its iteration (no score
+  // block computed ahead) with every K and V fragment read from LDS one
+  // contraction step before its use, which leaves room for four waves per SIMD
+  // at D = 64 (110 registers) and three at D = 128.  Split grids compute
+  // S(j+1) while the softmax of S(j) runs.
+  constexpr bool LEANF = SPLIT == 1;
   constexpr int NEED = LEANF ? 0 : 1;  // iteration i reads the tiles of iterations i .. i+NEED
   constexpr int GROUP = ring_group(SPLIT, NB, NEED, kFwdGroup);  // iterations per barrier
   static_assert(!LEANF || SPLIT * NB * SET <= 65536, "tile reads reach every slot by immediate offset");
   ring_prologue<NB, GROUP>(L, dma);
   Frag128 fo;
-  if constexpr (LEANF) fo.init(r, h, lane);
+  if constexpr (LEANF && D == 128) fo.init(r, h, lane);
+  auto rowf = [&](const char* t, int ks) -> MB::frag {  // K row fragment ks of tile t
+    if constexpr (D == 128) return fo.row_frag(t, ks);
+    else return read_row_frag<bf16, D>(t, r, ks, h);
+  };
+  auto trf = [&](const char* t, int ks, int dt) -> MB::frag {  // transposed V fragment
+    if constexpr (D == 128) return fo.trans(t, ks, dt);
+    else return TransRead<bf16, D>::read(t, 0, ks, dt * 32, lane);
+  };
   MB::frag qf[KS_D];
   load_row_frags<bf16, D>(Q + base, my_q, S, h, rs, qf);
   wait_vm(0);
@@ -216,10 +224,10 @@ void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K
         const char* kt = ring + sl * SET;
         f32x16 s = f32x16{};
         MB::frag ka[2];
-        ka[0] = fo.row_frag(kt, 0);
+        ka[0] = rowf(kt, 0);
 #pragma unroll
         for (int ks = 0; ks < KS_D; ++ks) {
-          if (ks + 1 < KS_D) ka[(ks + 1) & 1] = fo.row_frag(kt, ks + 1);
+          if (ks + 1 < KS_D) ka[(ks + 1) & 1] = rowf(kt, ks + 1);
           s = MB::run(ka[ks & 1], qf[ks], s);
         }
         if (CAUSAL && kNoClamp ? i >= i_mask : i == i_mask) {
@@ -248,13 +256,13 @@ void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K
         lsum += psum;
         const MB::frag pb[2] = {MB::pack(pv, 0), MB::pack(pv, 1)};
         MB::frag va[2];
-        va[0] = fo.trans(kt + TILE, 0, 0);
+        va[0] = trf(kt + TILE, 0, 0);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) {
             const int x = ks * DT + dt;
-            if (x + 1 < 2 * DT) va[(x + 1) & 1] = fo.trans(kt + TILE, (x + 1) / DT, (x + 1) % DT);
+            if (x + 1 < 2 * DT) va[(x + 1) & 1] = trf(kt + TILE, (x + 1) / DT, (x + 1) % DT);
             oacc[dt] = MB::run(va[x & 1], pb[ks], oacc[dt]);
           }
         return;
