@@ -399,8 +399,9 @@ void attn_fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K
 // dS = P (dP - D) takes one multiply per element: the dP contraction starts
 // from an accumulator holding D and multiplies by -dO, so it yields D - dP.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
-__global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG, bool STR>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(STR ? 4 : 1, 10)))
+void attn_bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                                                                const bf16* __restrict__ V, const bf16* __restrict__ O,
                                                                const bf16* __restrict__ dO,
                                                                const float* __restrict__ LSE, bf16* __restrict__ dQ,
@@ -497,6 +498,15 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
   const char* ring = smem + part * NB * SET;  // this wave's part
+  // STR (unsplit grids at D = 64 with at least four work groups per CU):
+  // every K, V and K^T fragment is read one contraction step before its use
+  // instead of a whole tile's at once, and D is broadcast into the dP
+  // accumulator in each iteration; the registers that saves give four waves
+  // per SIMD (124 registers).  Grids of up to about three work groups per CU
+  // run faster with the whole-tile reads at three waves per SIMD.
+  static_assert(!STR || (SPLIT == 1 && D == 64), "streamed form: unsplit, D = 64");
+  auto rowf = [&](const char* t, int ks) { return read_row_frag<bf16, D>(t, r, ks, h); };
+  auto trf = [&](const char* t, int ks, int dt) { return TransRead<bf16, D>::read(t, 0, ks, dt * 32, lane); };
 
   for (int i0 = 0; i0 < L; i0 += NB) {
     unroll<NB>([&](auto slc) {
@@ -507,8 +517,53 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(const bf16* __res
       if (i >= cnt) return;  // wave-uniform: this wave is done, it only keeps the barriers
       const int j = tb + i;  // key tile of this iteration
       const char* cur = ring + sl * SET;
-      // this tile's rows are read here rather than one tile ahead: the 32
-      // registers that saves give three waves per SIMD at D = 64
+      if constexpr (STR) {
+        // D broadcast into the dP accumulator here, not kept in 16 registers
+        // across the loop (the empty asm stops the compiler from hoisting it)
+        float dq_ = Dq;
+        asm volatile("" : "+v"(dq_));
+        f32x16 s = f32x16{}, dx;
+#pragma unroll
+        for (int a = 0; a < 16; ++a) dx[a] = dq_;
+        MB::frag ka[2], va[2];
+        ka[0] = rowf(cur, 0);
+        va[0] = rowf(cur + TILE, 0);
+#pragma unroll
+        for (int ks = 0; ks < KS_D; ++ks) {
+          if (ks + 1 < KS_D) {
+            ka[(ks + 1) & 1] = rowf(cur, ks + 1);
+            va[(ks + 1) & 1] = rowf(cur + TILE, ks + 1);
+          }
+          s = MB::run(ka[ks & 1], qf[ks], s);
+          dx = MB::run(va[ks & 1], dof[ks], dx);  // D - dP^T
+        }
+        if (CAUSAL && kNoClamp ? i >= i_mask : i == i_mask) {
+          const int k0 = j * 32;
+#pragma unroll
+          for (int a = 0; a < 16; ++a) {
+            const int key = k0 + acc_row(a, h);
+            if ((RAG && key >= S) || (CAUSAL && key > my_q)) s[a] = kMasked;
+          }
+        }
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          const float p = exp2_hw(fmaf(s[a], c, -lse2));
+          dx[a] = -p * dx[a];  // dS^T = P (dP - D)
+        }
+        const MB::frag db[2] = {MB::pack(dx, 0), MB::pack(dx, 1)};
+        MB::frag ta[2];
+        ta[0] = trf(cur, 0, 0);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const int x = ks * DT + dt;
+            if (x + 1 < 2 * DT) ta[(x + 1) & 1] = trf(cur, (x + 1) / DT, (x + 1) % DT);
+            dqacc[dt] = MB::run(ta[x & 1], db[ks], dqacc[dt]);
+          }
+        return;
+      }
+      // split grids read the whole tile's fragments here
       MB::frag kf[KS_D], vfr[KS_D];
       read_rows<D>(cur, r, h, kf);
       read_rows<D>(cur + TILE, r, h, vfr);
@@ -908,15 +963,24 @@ template <int D> struct BwdCfg {
   static constexpr int NB = D == 64 ? kBwdNb64 : kBwdNb128;
 };
 
+template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG, bool STR>
+static hipError_t launch_dq_t(const BwdArgs& a, float c, int n_qtiles, hipStream_t st) {
+  hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG, STR>),
+                     dim3((unsigned)((int64_t)a.BH * n_qtiles)), dim3(256), 0, st, (const bf16*)a.q,
+                     (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o, (const bf16*)a.dout, a.lse, (bf16*)a.dq,
+                     a.ws, a.S, a.BH, n_qtiles, c, a.scale, cu_count(), a.H, (int)a.seq_major);
+  return hipGetLastError();
+}
+
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>
 static hipError_t launch_dq(const BwdArgs& a, float c, hipStream_t st) {
   constexpr int BQ = 128 / SPLIT;
   const int n_qtiles = (a.S + BQ - 1) / BQ;
-  hipLaunchKernelGGL((attn_bwd_dq_bf16_kernel<D, CAUSAL, SPLIT, NB, RAG>), dim3((unsigned)((int64_t)a.BH * n_qtiles)),
-                     dim3(256), 0, st, (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, (const bf16*)a.o,
-                     (const bf16*)a.dout, a.lse, (bf16*)a.dq, a.ws, a.S, a.BH, n_qtiles, c, a.scale, cu_count(), a.H,
-                     (int)a.seq_major);
-  return hipGetLastError();
+  if constexpr (D == 64 && SPLIT == 1) {
+    if ((int64_t)a.BH * n_qtiles >= 4 * (int64_t)cu_count())
+      return launch_dq_t<D, CAUSAL, SPLIT, NB, RAG, true>(a, c, n_qtiles, st);
+  }
+  return launch_dq_t<D, CAUSAL, SPLIT, NB, RAG, false>(a, c, n_qtiles, st);
 }
 
 template <int D, bool CAUSAL, int SPLIT, int NB, bool RAG>

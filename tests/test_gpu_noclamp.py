@@ -28,6 +28,7 @@ CASES = [
     # B, H, S, D, sigma
     (8, 12, 1024, 64, 1.0),   # GPT-2 small
     (4, 24, 1000, 64, 1.0),   # ragged end
+    (4, 32, 1000, 64, 1.0),   # 1024 work groups: the dQ kernel's streamed four-wave form
     (1, 2, 300, 128, 1.0),    # small grid, ragged end
     (1, 2, 384, 128, 3.0),    # peaked softmax
 ]
