@@ -236,6 +236,21 @@ def test_extreme_scales(cuda, case):
     print("  " + "  ".join(rep + [f"lse maxabs={lse_err:.2e} (bound {lse_tol:.2e})"]), flush=True)
 
 
+def test_heads_independent_of_grid(cuda):
+    """A head's results do not depend on the rest of the batch: B = 8, H = 16
+    (1024 work groups per kernel: the dQ kernel's streamed four-wave form, the
+    dK/dV grid in plain heaviest-first order) and its first six batches alone
+    (768 work groups: the whole-tile dQ, the banded dK/dV order) agree bit for
+    bit.  (Grids under 768 work groups split the forward's key range, which
+    changes the summation order.)"""
+    q, k, v, do = make_inputs(8, 16, 1024, 64, "bf16", seed=2718)
+    say("grid independence B8 H16 S1024 vs B6")
+    full = gpu_fwd_bwd(q, k, v, do, 0.125, True)
+    part = gpu_fwd_bwd(q[:6], k[:6], v[:6], do[:6], 0.125, True)
+    for n, f, h in zip(("o", "lse", "dq", "dk", "dv"), full, part):
+        assert torch.equal(f[:6], h), f"{n}: batches 0-5 differ between the 8-batch and 6-batch grids"
+
+
 def test_deterministic(cuda):
     """No atomics: two runs give bitwise identical outputs."""
     w = WORKLOADS[1]
