@@ -68,8 +68,11 @@ def test_bshd_matches_bhsd_and_oracle(cuda, case):
         check_tensor(n, dtype, g.cpu(), r)
 
 
-def test_bshd_gpt2_small_full_size(cuda):
-    w = BY_NAME["gpt2_small_B8_H12_S1024_D64"]
+@pytest.mark.parametrize("name", ["gpt2_small_B8_H12_S1024_D64", "long_ctx_B2_H16_S4096_D128"])
+def test_bshd_full_size(cuda, name):
+    """Full-size workloads (D = 64 and D = 128, whose kernels address their
+    LDS fragments differently) in both storage orders: bit for bit equal."""
+    w = BY_NAME[name]
     say(f"layout bshd full {w.name}")
     dev = [t.to(DEV) for t in workload_inputs(w)]
     ref = run(*dev, w.scale, w.causal, "bhsd")
